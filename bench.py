@@ -1,0 +1,243 @@
+#!/usr/bin/env python3
+"""Benchmark: one decode step of 4-bit linears at batch 1 on one MI355X.
+
+Workload: a 3B-class decode step -- 28 layers x (qkv 5120x3072, o 3072x3072,
+gate_up 16384x3072, down 3072x8192) + lm_head 128256x3072, all symmetric
+4-bit with groups of 32 and fp16 scales, fp16 activations, M = 1: 113 linears
+and 1,809,859,072 bytes of weights, scales, x and y per step.  Weights are
+seeded N(0, 0.02^2), generated and packed on the device; x ~ N(0, 1) per
+linear.  A step is one wq_decode_linears call over all 113 linears, with every
+input already resident in HBM.
+
+Prints ONE JSON line: value = achieved GB/s of algorithmic bytes per step.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "achieved HBM GB/s (% of peak) & µs per decode step of 4-bit linears, batch 1"
+
+
+def parse_args():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--seed", type=int, default=1234)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="approximate CPU time budget of the oracle baseline sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="also run a plain device copy of this many MiB (for scaling HBM counters)")
+    return ap.parse_args()
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def build_step(seed, device):
+    import torch
+
+    from paper_2412_15803_amd import workloads as wl
+    from paper_2412_15803_amd import wq
+
+    plan = wl.decode_step_linears(base_seed=seed)
+    lins = []
+    total_bytes = 0
+    for lin, ws, xs in plan:
+        w = wl.weights_device(ws, lin.n, lin.k, device)
+        packed = torch.empty((lin.n, lin.k // 8), dtype=torch.int32, device=device)
+        scales = torch.empty((lin.n, lin.k // 32), dtype=torch.float16, device=device)
+        wq.wq_pack(w, packed, scales)
+        del w
+        x = wl.x_device(xs, 1, lin.k, device)
+        y = torch.empty((1, lin.n), dtype=torch.float16, device=device)
+        lins.append((packed, scales, x, y))
+        total_bytes += wl.ideal_bytes(lin.n, lin.k, 1)
+    torch.cuda.synchronize()
+    return plan, lins, total_bytes
+
+
+def per_launch_times(plan, lins, reps):
+    """Average duration of each linear's kernel, from HIP events recorded on
+    the launch stream between consecutive launches of the same sequence."""
+    import torch
+
+    from paper_2412_15803_amd import wq
+
+    n = len(lins)
+    acc = [0.0] * n
+    for _ in range(reps):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+        ev[0].record()
+        for i, (p, s, x, y) in enumerate(lins):
+            wq.wq_gemv(p, s, x, y)
+            ev[i + 1].record()
+        ev[-1].synchronize()
+        for i in range(n):
+            acc[i] += ev[i].elapsed_time(ev[i + 1])
+    return [a / reps for a in acc]
+
+
+def cpu_baseline(seed, budget_s):
+    """The oracle GEMV (as it stands) on a bounded prefix of the same step:
+    layer 0's four linears and the lm_head first, then further layers until
+    the time budget is spent.  Inputs are random packed words and scales of
+    the same shapes (the GEMV's cost does not depend on the values)."""
+    import numpy as np
+
+    sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+    import oracle
+    from paper_2412_15803_amd import workloads as wl
+
+    plan = wl.decode_step_linears(base_seed=seed)
+    order = plan[:4] + [plan[-1]] + plan[4:-1]
+    done_bytes = 0
+    done = []
+    t_total = 0.0
+    for lin, ws, xs in order:
+        p = wl.random_words_host(ws, lin.n, lin.k)
+        s = wl.random_scales_host(ws + 1, lin.n, lin.k)
+        x = wl.x_host(xs, 1, lin.k)
+        t0 = time.perf_counter()
+        oracle.gemv(p, s, x, lin.n, lin.k)
+        t_total += time.perf_counter() - t0
+        done_bytes += wl.ideal_bytes(lin.n, lin.k, 1)
+        done.append(lin.name)
+        if t_total >= budget_s and len(done) >= 5:
+            break
+    return {
+        "value": round(done_bytes / t_total / 1e9, 4),
+        "unit": "GB/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"{len(done)} of 113 linears of the same step ({done[0]} .. {done[-1]}, incl. lm_head), "
+                  f"{done_bytes / 1e9:.3f} GB in {t_total:.1f} s; NumPy elementwise + fp64 sums, one thread "
+                  f"(host {platform.processor() or platform.machine()}, {len(os.sched_getaffinity(0))} cores available)",
+    }
+
+
+def copy_probe(mib, device):
+    import torch
+
+    n = mib * (1 << 20) // 4
+    a = torch.ones(n, dtype=torch.float32, device=device)
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    b.copy_(a)
+    torch.cuda.synchronize()
+    log(f"copy probe: {mib} MiB read + {mib} MiB written")
+
+
+def main():
+    args = parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures the single-GPU decode linears only; runs on more than one GPU are not "
+              "part of this build (use --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2412_15803_amd import wq
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    device = torch.device("cuda:0")
+    wq.lib()  # fail loudly if the HIP library is missing
+
+    log("building the 3B-class decode step (113 linears) on the device")
+    plan, lins, step_bytes = build_step(args.seed, device)
+    arr = wq.make_linear_array(lins, 1)
+
+    if args.copy_probe_mib:
+        copy_probe(args.copy_probe_mib, device)
+
+    log(f"warmup {args.warmup} steps")
+    for _ in range(args.warmup):
+        wq.wq_decode_linears(lins, m=1, _array=arr)
+    torch.cuda.synchronize()
+
+    log(f"timing {args.steps} steps")
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(args.steps):
+        wq.wq_decode_linears(lins, m=1, _array=arr)
+    end.record()
+    torch.cuda.synchronize()
+    ms_per_step = start.elapsed_time(end) / args.steps
+    gbs = step_bytes / (ms_per_step * 1e-3) / 1e9
+
+    # Roofline of the dominant kernel: per-launch durations from events on the
+    # launch stream, grouped by kernel shape class (K decides the instantiation).
+    from paper_2412_15803_amd import workloads as wl
+
+    times = per_launch_times(plan, lins, reps=max(3, min(20, args.steps // 10)))
+    classes = {}
+    for (lin, _, _), t in zip(plan, times):
+        key = lin.k
+        c = classes.setdefault(key, {"ms": 0.0, "bytes": 0, "launches": 0})
+        c["ms"] += t
+        c["bytes"] += wl.ideal_bytes(lin.n, lin.k, 1)
+        c["launches"] += 1
+    dom_k, dom = max(classes.items(), key=lambda kv: kv[1]["ms"])
+    avg_ms = dom["ms"] / dom["launches"]
+    avg_bytes = dom["bytes"] / dom["launches"]
+    achieved = avg_bytes / (avg_ms * 1e-3) / 1e9
+    roofline = {
+        "bound": "hbm",
+        "achieved": round(achieved, 1),
+        "peak": HBM_PEAK_GBS,
+        "unit": "GB/s",
+        "frac": round(achieved / HBM_PEAK_GBS, 4),
+        "traffic": None,
+        "kernel": f"gemv_m1 (K={dom_k}: {dom['launches']} launches per step, avg {avg_ms * 1e3:.2f} us, "
+                  f"{avg_bytes / 1e6:.2f} MB algorithmic per launch)",
+    }
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log(f"timing the CPU oracle (~{args.cpu_seconds:.0f} s sample)")
+        cpu = cpu_baseline(args.seed, args.cpu_seconds)
+
+    out = {
+        "metric": METRIC,
+        "value": round(gbs, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "us_per_step": round(ms_per_step * 1e3, 2),
+        "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
+        "tokens_per_s_upper_bound": round(1e3 / ms_per_step, 1),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {
+            "workload": "3B-class decode step, batch 1: 28 x (qkv 5120x3072, o 3072x3072, gate_up 16384x3072, "
+                        "down 3072x8192) + lm_head 128256x3072; int4 g32 fp16 scales; 113 linears",
+            "batch_m": 1,
+            "linears": len(lins),
+            "bytes_per_step": step_bytes,
+        },
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

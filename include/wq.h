@@ -1,0 +1,139 @@
+/*
+ * wq.h -- C ABI of the MI355X (gfx950) 4-bit group-quantized decode-linear
+ * library.
+ *
+ * The operation is the decode-step linear layer of a 4-bit weight-quantized
+ * decoder LLM (WebLLM, Sec. 1 and Sec. 3 / Table 1: token-by-token decoding
+ * of 4-bit quantized 1-8B models; Sec. 2.3: weights converted ahead of time,
+ * dequantization fused into the matrix-vector kernel):
+ *
+ *     y[m][n] = sum_k x[m][k] * w_hat[n][k],   w_hat[n][k] = s16[n][k/32] * (q[n][k] - 8)
+ *
+ * Weight format (this library's reading of "4-bit quantized"):
+ *   - W is [N][K] (output features x input features), row-major.
+ *   - K is split into groups of 32 consecutive elements of a row.
+ *   - scale: s16 = fp16_rne(fp32(max|w over group| / 7)), stored as IEEE
+ *     binary16 bit patterns, [N][K/32] row-major.
+ *   - code: q = clamp(round_half_even(fp32(w / fp32(s16))) + 8, 0, 15);
+ *     q = 8 for every element when s16 == 0.
+ *   - packing: 8 codes per uint32, little-endian nibbles: element 8j+i of a
+ *     row is bits [4i, 4i+4) of word j; packed_w is [N][K/8] row-major.
+ * Activations x [M][K] and outputs y [M][N] are row-major IEEE binary16
+ * passed as uint16_t bit patterns.
+ *
+ * Conventions shared by every entry point:
+ *   - All data pointers are DEVICE pointers, allocated and owned by the
+ *     caller.  The library keeps no reference to them after the call returns
+ *     (wq_decode_linears copies the descriptor array, see there).
+ *   - `stream` is a hipStream_t passed as void*; NULL is the null stream.
+ *     Calls are asynchronous and stream-ordered: they return after queuing
+ *     work.  A device fault surfaces at the caller's next synchronization.
+ *   - Every argument is validated on the host BEFORE any HIP call, so an
+ *     invalid call returns an error without touching the device.
+ *   - Return values are wq_status codes; wq_last_error_message() gives a
+ *     human-readable description of the last failure on the calling thread.
+ *   - Non-finite weights or activations give unspecified (but memory-safe)
+ *     results.
+ */
+#ifndef WQ_H
+#define WQ_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum wq_status {
+    WQ_OK = 0,
+    WQ_ERR_INVALID_ARG = 1,  /* null pointer, size <= 0 or too large, aliasing */
+    WQ_ERR_UNSUPPORTED = 2,  /* group != 32, K % 32 != 0 */
+    WQ_ERR_MISALIGNED = 3,   /* a pointer below its required alignment */
+    WQ_ERR_HIP = 4           /* the HIP runtime reported an error */
+} wq_status;
+
+/* Largest accepted sizes. */
+#define WQ_MAX_N ((int64_t)0x7fffffff)
+#define WQ_MAX_K ((int64_t)0x7fffffe0)
+#define WQ_MAX_M ((int64_t)65535)
+#define WQ_MAX_LINEARS ((int64_t)65536)
+
+/* Static string naming a status code ("WQ_OK", ...); "WQ_UNKNOWN_STATUS" for
+ * values outside the enum.  Never NULL. */
+const char* wq_status_string(int status);
+
+/* Description of the last non-OK status returned on the calling thread
+ * (thread-local, overwritten by the next failing call).  Never NULL. */
+const char* wq_last_error_message(void);
+
+/* Library ABI version: 100 * major + minor. */
+int wq_version(void);
+
+/*
+ * wq_pack -- quantize fp32 weights to the 4-bit format above (the ahead-of-
+ * time weight conversion of Sec. 2.3; 4-bit models of Table 1).
+ *
+ *   w         [N][K] fp32, device, 16-byte aligned, read only.
+ *   packed_w  [N][K/8] uint32, device, 16-byte aligned, written.
+ *   scales    [N][K/32] fp16 bits, device, 2-byte aligned, written.
+ *   N, K      1 <= N <= WQ_MAX_N, 32 <= K <= WQ_MAX_K.
+ *   group     must be 32.
+ * Output is bit-exact: IEEE division, round-half-even, fp16 subnormals kept.
+ * Errors: INVALID_ARG (null, N or K <= 0 or too large, output overlapping w),
+ *         UNSUPPORTED (group != 32, K % 32 != 0), MISALIGNED, HIP.
+ */
+wq_status wq_pack(const float* w, uint32_t* packed_w, uint16_t* scales,
+                  int64_t N, int64_t K, int64_t group, void* stream);
+
+/*
+ * wq_gemv -- y = x * dequant(W)^T for a small batch of activations (the
+ * decode-step linear, Sec. 1 / Table 1; dequantization fused in registers).
+ *
+ *   packed_w  [N][K/8] uint32, device, 16-byte aligned, read only.
+ *   scales    [N][K/32] fp16 bits, device, 2-byte aligned, read only.
+ *   x         [M][K] fp16 bits, device, 16-byte aligned, read only.
+ *   y         [M][N] fp16 bits, device, 2-byte aligned, written.
+ *   N, K, M   1 <= N <= WQ_MAX_N, 32 <= K <= WQ_MAX_K, 1 <= M <= WQ_MAX_M.
+ *   group     must be 32.
+ * Accumulation is fp32 with exact products; each output is rounded once to
+ * fp16 (round to nearest even).  Per element the result is within
+ * 1e-3 * sum_k |w_hat[n][k] x[m][k]| + 1e-5 of the exactly rounded value.
+ * y must not overlap x, packed_w or scales.
+ * Errors: INVALID_ARG, UNSUPPORTED, MISALIGNED, HIP (as for wq_pack).
+ */
+wq_status wq_gemv(const uint32_t* packed_w, const uint16_t* scales,
+                  const uint16_t* x, uint16_t* y,
+                  int64_t N, int64_t K, int64_t M, int64_t group, void* stream);
+
+/* One linear layer of a decode step; pointers and sizes as for wq_gemv. */
+typedef struct wq_linear {
+    const uint32_t* packed_w;
+    const uint16_t* scales;
+    const uint16_t* x;
+    uint16_t* y;
+    int64_t N;
+    int64_t K;
+} wq_linear;
+
+/*
+ * wq_decode_linears -- run linears[0 .. count) in order on one stream: one
+ * decode step's linear layers (the per-token work whose throughput Table 1
+ * reports).  Linear i may read, as its x, the y written by any linear j < i,
+ * and may overwrite any earlier linear's x or y: the result is that of
+ * running the linears one after another.  No y may overlap the x of the
+ * same linear, nor the packed_w or scales of any linear in the list.
+ *
+ *   linears   HOST array of `count` descriptors; copied during the call, so
+ *             it may be freed or reused as soon as the call returns.
+ *   count     1 <= count <= WQ_MAX_LINEARS.
+ *   M, group  shared by all linears (1 <= M <= WQ_MAX_M, group == 32).
+ * Errors: as wq_gemv, checked for every descriptor before anything runs.
+ */
+wq_status wq_decode_linears(const wq_linear* linears, int64_t count,
+                            int64_t M, int64_t group, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WQ_H */

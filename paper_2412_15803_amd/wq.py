@@ -1,0 +1,178 @@
+"""Thin ctypes binding of the C ABI in include/wq.h.
+
+Only argument marshalling happens here: torch tensors are turned into device
+pointers and sizes, the current HIP stream is passed through, and non-OK
+status codes become WQError.  Every step of the computation runs in the HIP
+library; if the library is not built this module raises instead of falling
+back to anything else.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "lib", "libwq.so")
+
+WQ_OK = 0
+WQ_ERR_INVALID_ARG = 1
+WQ_ERR_UNSUPPORTED = 2
+WQ_ERR_MISALIGNED = 3
+WQ_ERR_HIP = 4
+
+GROUP = 32
+
+# Every function declared in include/wq.h.
+EXPORTED = ("wq_status_string", "wq_last_error_message", "wq_version", "wq_pack", "wq_gemv",
+            "wq_decode_linears")
+
+
+class WqLinear(ctypes.Structure):
+    _fields_ = [
+        ("packed_w", ctypes.c_void_p),
+        ("scales", ctypes.c_void_p),
+        ("x", ctypes.c_void_p),
+        ("y", ctypes.c_void_p),
+        ("N", ctypes.c_int64),
+        ("K", ctypes.c_int64),
+    ]
+
+
+class WQError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{status_string(status)}: {message}")
+        self.status = status
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libwq.so (once) and declare the C signatures."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"HIP library not built: {LIB_PATH} is missing "
+                           "(run `python -m paper_2412_15803_amd.build`)")
+    L = ctypes.CDLL(LIB_PATH)
+    i64, vp = ctypes.c_int64, ctypes.c_void_p
+    L.wq_status_string.argtypes = [ctypes.c_int]
+    L.wq_status_string.restype = ctypes.c_char_p
+    L.wq_last_error_message.argtypes = []
+    L.wq_last_error_message.restype = ctypes.c_char_p
+    L.wq_version.argtypes = []
+    L.wq_version.restype = ctypes.c_int
+    L.wq_pack.argtypes = [vp, vp, vp, i64, i64, i64, vp]
+    L.wq_pack.restype = ctypes.c_int
+    L.wq_gemv.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, vp]
+    L.wq_gemv.restype = ctypes.c_int
+    L.wq_decode_linears.argtypes = [ctypes.POINTER(WqLinear), i64, i64, i64, vp]
+    L.wq_decode_linears.restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def status_string(status: int) -> str:
+    return lib().wq_status_string(int(status)).decode()
+
+
+def last_error_message() -> str:
+    return lib().wq_last_error_message().decode()
+
+
+def _check(status: int) -> None:
+    if status != WQ_OK:
+        raise WQError(status, last_error_message())
+
+
+# ------------------------------------------------------------- marshalling
+
+def _dev_tensor(t, name, dtypes, shape):
+    import torch
+
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a device tensor (got {t.device})")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected one of {dtypes}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous (row-major)")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream, device):
+    import torch
+
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _word_dtypes():
+    import torch
+
+    return (torch.int32, torch.uint32)
+
+
+def _half_dtypes():
+    import torch
+
+    return (torch.float16, torch.int16, torch.uint16)
+
+
+def wq_pack(w, packed_w, scales, group: int = GROUP, stream=None) -> None:
+    """Quantize fp32 w [N, K] into packed_w [N, K/8] (int32/uint32 words) and
+    scales [N, K/32] (fp16), both preallocated on the same device."""
+    import torch
+
+    if w.dim() != 2:
+        raise ValueError("w must be 2-D [N, K]")
+    n, k = w.shape
+    pw = _dev_tensor(w, "w", (torch.float32,), (n, k))
+    pp = _dev_tensor(packed_w, "packed_w", _word_dtypes(), (n, k // 8))
+    ps = _dev_tensor(scales, "scales", _half_dtypes(), (n, k // group if group else 0))
+    _check(lib().wq_pack(pw, pp, ps, n, k, group, _stream(stream, w.device)))
+
+
+def wq_gemv(packed_w, scales, x, y, group: int = GROUP, stream=None) -> None:
+    """y [M, N] = x [M, K] . dequant(packed_w, scales)^T (fp16 in, fp16 out)."""
+    if x.dim() != 2 or packed_w.dim() != 2:
+        raise ValueError("x must be [M, K] and packed_w [N, K/8]")
+    m, k = x.shape
+    n = packed_w.shape[0]
+    pp = _dev_tensor(packed_w, "packed_w", _word_dtypes(), (n, k // 8))
+    ps = _dev_tensor(scales, "scales", _half_dtypes(), (n, k // group if group else 0))
+    px = _dev_tensor(x, "x", _half_dtypes(), (m, k))
+    py = _dev_tensor(y, "y", _half_dtypes(), (m, n))
+    _check(lib().wq_gemv(pp, ps, px, py, n, k, m, group, _stream(stream, x.device)))
+
+
+def make_linear_array(linears, m: int, group: int = GROUP):
+    """Marshal a sequence of (packed_w, scales, x, y) tensor tuples into a
+    ctypes wq_linear array."""
+    arr = (WqLinear * len(linears))()
+    for i, (packed_w, scales, x, y) in enumerate(linears):
+        if x.dim() != 2 or x.shape[0] != m:
+            raise ValueError(f"linear {i}: x must be [M={m}, K]")
+        k = x.shape[1]
+        n = packed_w.shape[0]
+        arr[i].packed_w = _dev_tensor(packed_w, f"linears[{i}].packed_w", _word_dtypes(), (n, k // 8)).value
+        arr[i].scales = _dev_tensor(scales, f"linears[{i}].scales", _half_dtypes(), (n, k // group if group else 0)).value
+        arr[i].x = _dev_tensor(x, f"linears[{i}].x", _half_dtypes(), (m, k)).value
+        arr[i].y = _dev_tensor(y, f"linears[{i}].y", _half_dtypes(), (m, n)).value
+        arr[i].N = n
+        arr[i].K = k
+    return arr
+
+
+def wq_decode_linears(linears, m: int = 1, group: int = GROUP, stream=None, _array=None) -> None:
+    """Run a decode step's linears in order on one stream.  `linears` is a
+    sequence of (packed_w, scales, x, y) tuples; a prebuilt array from
+    make_linear_array may be passed as _array to skip re-marshalling."""
+    arr = _array if _array is not None else make_linear_array(linears, m, group)
+    device = linears[0][2].device
+    _check(lib().wq_decode_linears(arr, len(arr), m, group, _stream(stream, device)))
