@@ -1,0 +1,265 @@
+"""wq_decode_linears on the GPU: the persistent decode-step kernel (M = 1,
+K <= 16384) and the per-linear fallback, against the CPU oracle.
+
+Outputs are pre-filled with NaN and every row is checked, so a tile that is
+never computed shows up.  Integer-valued data (unit scales, codes in
+{7, 8, 9}, x in {-1, 0, 1}) keeps every partial sum an exact integer in
+fp32, so results are unique and compared bit for bit, also along chains of
+dependent linears.
+"""
+
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import announce, require_gpu, to_dev, to_host
+from paper_2412_15803_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    require_gpu()
+
+
+def int_linear(rng, n, k, p_nonzero=1 / 8):
+    """Packed words and unit scales for codes in {7, 8, 9}."""
+    p = p_nonzero / 2
+    codes = rng.choice([7, 8, 9], size=(n, k), p=[p, 1 - 2 * p, p])
+    packed = np.zeros((n, k // 8), dtype=np.uint32)
+    for b in range(8):
+        packed |= codes[:, b::8].astype(np.uint32) << np.uint32(4 * b)
+    return packed, wl.constant_scales_host(n, k, 0x3C00)
+
+
+def nan_out(m, n):
+    import torch
+
+    return torch.full((m, n), float("nan"), dtype=torch.float16, device="cuda")
+
+
+def run(lins, m=1, stream=None):
+    import torch
+
+    from paper_2412_15803_amd import wq
+
+    wq.wq_decode_linears(lins, m=m, stream=stream)
+    torch.cuda.synchronize()
+
+
+def check_exact(y_dev, y_ref, what):
+    yh = to_host(y_dev, np.float16)
+    bad = np.argwhere(yh.view(np.uint16) != y_ref.view(np.uint16))
+    assert bad.size == 0, f"{what}: {len(bad)} mismatches, first {bad[:4].tolist()}"
+
+
+def test_independent_linears_mixed_k_bit_exact():
+    """Independent linears of every groups-per-lane class (K from 32 to
+    16384), ragged row counts, one call."""
+    rng = np.random.default_rng(1)
+    shapes = [(37, 32), (1000, 512), (513, 2048), (300, 3072), (129, 4096), (77, 6144), (64, 8192),
+              (50, 10240), (33, 14336), (17, 16384), (4097, 3072)]
+    announce("decode independent mixed K")
+    host, lins = [], []
+    for n, k in shapes:
+        p, s = int_linear(rng, n, k, 1 / 4)
+        x = rng.integers(-1, 2, size=(1, k)).astype(np.float16)
+        host.append((p, s, x))
+        lins.append((to_dev(p), to_dev(s), to_dev(x), nan_out(1, n)))
+    run(lins)
+    for (p, s, x), (_, _, _, y), (n, k) in zip(host, lins, shapes):
+        check_exact(y, oracle.gemv(p, s, x, n, k), f"{n}x{k}")
+
+
+def test_small_k_only_uses_narrow_kernel_bit_exact():
+    rng = np.random.default_rng(2)
+    shapes = [(5120, 3072), (3072, 3072), (16384, 3072), (3072, 8192)]
+    announce("decode 3B layer shapes, integer data")
+    host, lins = [], []
+    for n, k in shapes:
+        p, s = int_linear(rng, n, k)
+        x = rng.integers(-1, 2, size=(1, k)).astype(np.float16)
+        host.append((p, s, x))
+        lins.append((to_dev(p), to_dev(s), to_dev(x), nan_out(1, n)))
+    run(lins)
+    for (p, s, x), (_, _, _, y), (n, k) in zip(host, lins, shapes):
+        check_exact(y, oracle.gemv(p, s, x, n, k), f"{n}x{k}")
+
+
+def _chain_ref(layers, x0):
+    outs, x = [], x0
+    for p, s in layers:
+        y = oracle.gemv(p, s, x, p.shape[0], p.shape[1] * 8)
+        outs.append(y)
+        x = y
+    return outs
+
+
+def test_long_dependency_chain_bit_exact():
+    """x of linear i+1 is y of linear i for 40 linears of varying widths."""
+    rng = np.random.default_rng(3)
+    dims = [int(d) for d in rng.choice([256, 512, 1024, 2048, 3072], size=41)]
+    layers = [int_linear(rng, dims[i + 1], dims[i], 1 / 16) for i in range(40)]
+    x0 = rng.integers(-1, 2, size=(1, dims[0])).astype(np.float16)
+    announce("decode 40-linear chain")
+    lins, x = [], to_dev(x0)
+    for p, s in layers:
+        y = nan_out(1, p.shape[0])
+        lins.append((to_dev(p), to_dev(s), x, y))
+        x = y
+    run(lins)
+    for i, (ref, lin) in enumerate(zip(_chain_ref(layers, x0), lins)):
+        check_exact(lin[3], ref, f"chain linear {i}")
+
+
+def test_write_after_read_and_three_way_conflicts():
+    """Linear 2 overwrites linear 0's input (write-after-read) and reads
+    linear 1's output; linear 4 conflicts with three earlier linears, which
+    switches the whole call to strict ordering."""
+    import torch
+
+    rng = np.random.default_rng(4)
+    k = n = 1024
+    L = [int_linear(rng, n, k, 1 / 16) for _ in range(5)]
+    xa = rng.integers(-1, 2, size=(1, k)).astype(np.float16)
+    buf_a = to_dev(xa)                # x of 0 and 1, overwritten by 2
+    y0, y1, y3 = nan_out(1, n), nan_out(1, n), nan_out(1, n)
+    big = torch.full((1, 3 * n), float("nan"), dtype=torch.float16, device="cuda")
+    y4 = big[:, :n]                    # written by 4; 4 reads a view spanning y0-like data
+    announce("decode WAR + 3-way conflicts")
+    lins = [
+        (to_dev(L[0][0]), to_dev(L[0][1]), buf_a, y0),
+        (to_dev(L[1][0]), to_dev(L[1][1]), buf_a, y1),
+        (to_dev(L[2][0]), to_dev(L[2][1]), y1, buf_a),   # reads y1, overwrites x of 0 and 1
+        (to_dev(L[3][0]), to_dev(L[3][1]), buf_a, y3),   # reads the new buf_a
+        (to_dev(L[4][0]), to_dev(L[4][1]), y3, y4),
+    ]
+    run(lins)
+    r0 = oracle.gemv(L[0][0], L[0][1], xa, n, k)
+    r1 = oracle.gemv(L[1][0], L[1][1], xa, n, k)
+    r2 = oracle.gemv(L[2][0], L[2][1], r1, n, k)
+    r3 = oracle.gemv(L[3][0], L[3][1], r2, n, k)
+    r4 = oracle.gemv(L[4][0], L[4][1], r3, n, k)
+    check_exact(y0, r0, "0")
+    check_exact(y1, r1, "1")
+    check_exact(buf_a, r2, "2 (overwrote the shared input)")
+    check_exact(y3, r3, "3")
+    check_exact(y4, r4, "4")
+
+    # Three conflicts for one linear: it reads y3 and overwrites y0 and y1.
+    rng2 = np.random.default_rng(5)
+    L5 = int_linear(rng2, 2 * n, k, 1 / 16)
+    both = torch.full((1, 2 * n), float("nan"), dtype=torch.float16, device="cuda")
+    lins2 = [
+        (to_dev(L[0][0]), to_dev(L[0][1]), buf_a, both[:, :n]),
+        (to_dev(L[1][0]), to_dev(L[1][1]), buf_a, both[:, n:]),
+        (to_dev(L[3][0]), to_dev(L[3][1]), buf_a, y3),
+        (to_dev(L5[0]), to_dev(L5[1]), y3, both),
+    ]
+    xb = to_host(buf_a, np.float16)
+    run(lins2)
+    r3b = oracle.gemv(L[3][0], L[3][1], xb, n, k)
+    check_exact(y3, r3b, "3b")
+    check_exact(both, oracle.gemv(L5[0], L5[1], r3b, 2 * n, k), "5 (three conflicts)")
+
+
+def test_repeated_and_alternating_calls():
+    """Counters reset between launches; switching descriptor lists re-uploads
+    the table; two streams each get their own workspace."""
+    import torch
+
+    rng = np.random.default_rng(6)
+    setA = [int_linear(rng, n, 2048, 1 / 8) for n in (700, 1300, 64)]
+    setB = [int_linear(rng, n, 3072, 1 / 8) for n in (2000, 96)]
+    xA = rng.integers(-1, 2, size=(1, 2048)).astype(np.float16)
+    xB = rng.integers(-1, 2, size=(1, 3072)).astype(np.float16)
+    dA, dB = to_dev(xA), to_dev(xB)
+    linsA = [(to_dev(p), to_dev(s), dA, nan_out(1, p.shape[0])) for p, s in setA]
+    linsB = [(to_dev(p), to_dev(s), dB, nan_out(1, p.shape[0])) for p, s in setB]
+    refA = [oracle.gemv(p, s, xA, p.shape[0], 2048) for p, s in setA]
+    refB = [oracle.gemv(p, s, xB, p.shape[0], 3072) for p, s in setB]
+    announce("decode repeated / alternating / two streams")
+    for rep in range(3):
+        for lins, refs in ((linsA, refA), (linsB, refB)):
+            for lin in lins:
+                lin[3].fill_(float("nan"))
+            run(lins)
+            for lin, r in zip(lins, refs):
+                check_exact(lin[3], r, f"rep {rep}")
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    for lin in linsA + linsB:
+        lin[3].fill_(float("nan"))
+    torch.cuda.synchronize()
+    from paper_2412_15803_amd import wq
+
+    wq.wq_decode_linears(linsA, m=1, stream=s1)
+    wq.wq_decode_linears(linsB, m=1, stream=s2)
+    torch.cuda.synchronize()
+    for lin, r in zip(linsA + linsB, refA + refB):
+        check_exact(lin[3], r, "two streams")
+
+
+def test_many_linears_grow_workspace():
+    rng = np.random.default_rng(7)
+    count = 300
+    shapes = [(int(rng.integers(1, 200)), int(rng.choice([32, 64, 256, 1024]))) for _ in range(count)]
+    announce(f"decode {count} small linears")
+    host, lins = [], []
+    for n, k in shapes:
+        p, s = int_linear(rng, n, k, 1 / 4)
+        x = rng.integers(-1, 2, size=(1, k)).astype(np.float16)
+        host.append((p, s, x))
+        lins.append((to_dev(p), to_dev(s), to_dev(x), nan_out(1, n)))
+    run(lins)
+    for (p, s, x), lin, (n, k) in zip(host, lins, shapes):
+        check_exact(lin[3], oracle.gemv(p, s, x, n, k), f"{n}x{k}")
+
+
+def test_fallback_paths_small_batch_and_long_k():
+    """M > 1 and K > 16384 run as one launch per linear, still in order."""
+    rng = np.random.default_rng(8)
+    announce("decode fallback M=4 chain and K=16416")
+    m = 4
+    a = int_linear(rng, 512, 1024, 1 / 16)
+    b = int_linear(rng, 256, 512, 1 / 16)
+    x0 = rng.integers(-1, 2, size=(m, 1024)).astype(np.float16)
+    ya, yb = nan_out(m, 512), nan_out(m, 256)
+    run([(to_dev(a[0]), to_dev(a[1]), to_dev(x0), ya), (to_dev(b[0]), to_dev(b[1]), ya, yb)], m=m)
+    ra = oracle.gemv(a[0], a[1], x0, 512, 1024)
+    check_exact(ya, ra, "M=4 first")
+    check_exact(yb, oracle.gemv(b[0], b[1], ra, 256, 512), "M=4 second")
+    c = int_linear(rng, 100, 16416, 1 / 16)
+    xc = rng.integers(-1, 2, size=(1, 16416)).astype(np.float16)
+    yc = nan_out(1, 100)
+    run([(to_dev(c[0]), to_dev(c[1]), to_dev(xc), yc)])
+    check_exact(yc, oracle.gemv(c[0], c[1], xc, 100, 16416), "K=16416")
+
+
+def test_decode_matches_single_gemv_random_data():
+    """On random fp data the persistent kernel gives the same bits as
+    wq_gemv for each linear (same per-row arithmetic), and both are within
+    tolerance of the oracle."""
+    import torch
+
+    from paper_2412_15803_amd import wq
+
+    rng = np.random.default_rng(9)
+    shapes = [(5120, 3072), (3072, 8192), (6144, 4096), (4096, 14336)]
+    announce("decode vs gemv, random data")
+    lins, singles, host = [], [], []
+    for i, (n, k) in enumerate(shapes):
+        p, s = wl.random_words_host(50 + i, n, k), wl.random_scales_host(70 + i, n, k)
+        x = wl.x_host(60 + i, 1, k)
+        host.append((p, s, x))
+        dp, ds, dx = to_dev(p), to_dev(s), to_dev(x)
+        lins.append((dp, ds, dx, nan_out(1, n)))
+        y1 = nan_out(1, n)
+        wq.wq_gemv(dp, ds, dx, y1)
+        singles.append(y1)
+    run(lins)
+    for (p, s, x), lin, y1, (n, k) in zip(host, lins, singles, shapes):
+        assert torch.equal(lin[3].view(torch.int16), y1.view(torch.int16)), f"{n}x{k}"
+        ok = oracle.within_tolerance(to_host(lin[3], np.float16), oracle.gemv(p, s, x, n, k),
+                                     oracle.tol_bound(p, s, x, n, k))
+        assert ok.all(), f"{n}x{k}"

@@ -267,12 +267,13 @@ def test_gemv_invalid_call_leaves_output_untouched():
     from paper_2412_15803_amd import wq
 
     announce("gemv invalid args")
-    packed = torch.zeros((64, 8), dtype=torch.int32, device="cuda")
-    scales = torch.zeros((64, 2), dtype=torch.float16, device="cuda")
-    x = torch.zeros((1, 64), dtype=torch.float16, device="cuda")
+    # K = 48 is not a multiple of the group size: the library refuses it.
+    packed = torch.zeros((64, 6), dtype=torch.int32, device="cuda")
+    scales = torch.zeros((64, 1), dtype=torch.float16, device="cuda")
+    x = torch.zeros((1, 48), dtype=torch.float16, device="cuda")
     y = torch.full((1, 64), 3.0, dtype=torch.float16, device="cuda")
     with pytest.raises(wq.WQError) as e:
-        wq.wq_gemv(packed, scales, x, y, group=64)
+        wq.wq_gemv(packed, scales, x, y)
     assert e.value.status == wq.WQ_ERR_UNSUPPORTED
     torch.cuda.synchronize()
     assert bool((y == 3.0).all())
