@@ -33,6 +33,9 @@ COMPILE_FLAGS = [
     "-Wno-unused-command-line-argument",
     # Keep the compiler from forming packed-fp32 instructions.
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # The ticket claims are issued by one lane on purpose and their results
+    # read much later; the wave-level atomic rewrite would wait right away.
+    "-mllvm", "-amdgpu-atomic-optimizer-strategy=None",
     "-I", INCLUDE,
     "-I", CSRC,
 ]

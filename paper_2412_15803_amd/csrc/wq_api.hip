@@ -6,11 +6,13 @@
 #include <cstdlib>
 #include <cstring>
 #include <map>
+#include <memory>
 #include <mutex>
 #include <utility>
 #include <vector>
 
 #include "wq.h"
+#include "wq_device.h"
 #include "wq_internal.h"
 
 namespace {
@@ -80,173 +82,259 @@ wq_status hip_status(const char* fn, hipError_t e) {
 
 
 // ------------------------------------------------------------ decode step
-//
-// Per (device, stream) workspace of the persistent decode kernel: the device
-// copy of the linear table, the counter words, and a pinned staging buffer
-// for table uploads.  Allocated on first use and kept until the process ends.
-struct DecodeWorkspace {
-    wq::DecodeEntry* d_table = nullptr;
-    uint32_t* d_sync = nullptr;
-    int capacity = 0;
-    wq::DecodeEntry* h_stage = nullptr;
-    hipEvent_t staged = nullptr;  // the last upload has been read by the device
-    bool stage_pending = false;
-    std::vector<wq::DecodeEntry> uploaded;
-    uint32_t spin_limit = 1u << 18;  // polls of a dependency counter before giving up
-    int blocks = 0;
+
+// A union of address intervals, kept merged, for the dependency checks.
+class SpanSet {
+  public:
+    bool hits(Span s) const {
+        if (s.lo >= s.hi) return false;
+        auto it = m_.lower_bound(s.hi);  // first interval starting at or after s.hi
+        if (it == m_.begin()) return false;
+        --it;                            // the interval with the largest start below s.hi
+        return it->second > s.lo;
+    }
+    void add(Span s) {
+        if (s.lo >= s.hi) return;
+        auto it = m_.upper_bound(s.lo);
+        if (it != m_.begin() && std::prev(it)->second >= s.lo) {
+            --it;
+            s.lo = it->first;
+            s.hi = std::max(s.hi, it->second);
+            it = m_.erase(it);
+        }
+        while (it != m_.end() && it->first <= s.hi) {
+            s.hi = std::max(s.hi, it->second);
+            it = m_.erase(it);
+        }
+        m_[s.lo] = s.hi;
+    }
+    void clear() { m_.clear(); }
+
+  private:
+    std::map<uintptr_t, uintptr_t> m_;  // lo -> hi
 };
 
-std::mutex g_ws_mu;
-std::map<std::pair<int, hipStream_t>, DecodeWorkspace*> g_ws;
+// Split the linears into consecutive groups in which no linear reads the
+// output of, or writes the input or output of, another linear of the same
+// group.  Groups run in stream order, so this reproduces running the linears
+// one after another.  Linears the grouped kernel cannot take (K > 16384) form
+// groups of their own.
+struct Group {
+    int begin, end;  // linear indices [begin, end)
+    bool grouped;    // run with the grouped kernel (else one GEMV launch)
+};
 
-// Target weight bytes per claimed tile: large for linears nothing waits on
-// (a wave drains its pipeline when it moves to another linear), small where
-// a dependency chain needs many waves on the same linear.
-constexpr int64_t kTileBytesFree = 96 * 1024;
-constexpr int64_t kTileBytesChained = 24 * 1024;
-
-int rows_per_step(int gpl) { return gpl >= 8 ? 1 : 8 / gpl; }
-
-// Build the kernel's view of the linears: tiling, dependencies, signals.
-bool plan_decode(const std::vector<wq_linear>& lin, std::vector<wq::DecodeEntry>& ents, int& total_tiles,
-                 int& max_gpl) {
+std::vector<Group> split_groups(const std::vector<wq_linear>& lin) {
+    std::vector<Group> groups;
+    SpanSet reads, writes;
     const int count = (int)lin.size();
-    ents.assign(count, wq::DecodeEntry{});
-    max_gpl = 1;
+    int begin = 0;
     for (int i = 0; i < count; ++i) {
-        wq::DecodeEntry& e = ents[i];
         const wq_linear& l = lin[i];
+        if (l.K / 32 > 64 * wq::kDecodeMaxGpl) {
+            if (i > begin) groups.push_back(Group{begin, i, true});
+            groups.push_back(Group{i, i + 1, false});
+            reads.clear();
+            writes.clear();
+            begin = i + 1;
+            continue;
+        }
+        const Span x = span_of(l.x, 2 * l.K), y = span_of(l.y, 2 * l.N);
+        if (i > begin && (writes.hits(x) || reads.hits(y) || writes.hits(y))) {
+            groups.push_back(Group{begin, i, true});
+            reads.clear();
+            writes.clear();
+            begin = i;
+        }
+        reads.add(x);
+        writes.add(y);
+    }
+    if (begin < count) groups.push_back(Group{begin, count, true});
+    return groups;
+}
+
+int rows_per_step(int lpr, int gpl) { return (gpl >= 8 ? 1 : 8 / gpl) * (64 / lpr); }
+
+size_t align16(size_t v) { return (v + 15) & ~size_t(15); }
+
+// Serialised plan of one grouped launch: [entries][classes][class list].
+struct GroupPlan {
+    size_t off_entries, off_classes, off_list;
+    int nclasses;
+    int max_gpl;
+    int waves;
+};
+
+// Append the plan of linears [g.begin, g.end) to `bytes`.  `capacity` is
+// the number of waves the device holds at once; classes get waves in
+// proportion to their bytes, at least one and at most one per step.
+GroupPlan plan_group(const std::vector<wq_linear>& lin, const Group& g, int capacity4, int capacity8,
+                     std::vector<unsigned char>& bytes) {
+    const int count = g.end - g.begin;
+    std::vector<wq::DecodeEntry> ents(count, wq::DecodeEntry{});
+    std::vector<wq::DecodeClass> cls;
+    std::vector<std::vector<int32_t>> members;
+    std::vector<double> work;
+    int max_gpl = 1;
+    for (int i = 0; i < count; ++i) {
+        const wq_linear& l = lin[g.begin + i];
+        wq::DecodeEntry& e = ents[i];
         e.packed = l.packed_w;
         e.scales = l.scales;
         e.x = l.x;
         e.y = l.y;
         e.n = l.N;
         e.ng = (int32_t)(l.K / 32);
-        e.gpl = (e.ng + 63) / 64;
-        max_gpl = std::max(max_gpl, (int)e.gpl);
-        e.dep0 = e.dep1 = -1;
-        e.signal = 0;
-    }
-    // Linear i must wait for every earlier linear j whose output it reads,
-    // whose input it overwrites, or whose output it overwrites.
-    bool chain = count > 4096;
-    for (int i = 0; i < count && !chain; ++i) {
-        const Span xi = span_of(lin[i].x, 2 * lin[i].K), yi = span_of(lin[i].y, 2 * lin[i].N);
-        int found = 0;
-        for (int j = i - 1; j >= 0; --j) {
-            const Span xj = span_of(lin[j].x, 2 * lin[j].K), yj = span_of(lin[j].y, 2 * lin[j].N);
-            if (overlaps(xi, yj) || overlaps(yi, xj) || overlaps(yi, yj)) {
-                if (found == 0) ents[i].dep0 = j;
-                else if (found == 1) ents[i].dep1 = j;
-                else chain = true;
-                ++found;
-            }
+        int lpr = 64, gpl = 1;
+        wq::dev::pick_shape(e.ng, lpr, gpl);
+        e.lpr = lpr;
+        e.gpl = gpl;
+        max_gpl = std::max(max_gpl, gpl);
+        int ci = 0;
+        while (ci < (int)cls.size() && !(cls[ci].lpr == lpr && cls[ci].gpl == gpl)) ++ci;
+        if (ci == (int)cls.size()) {
+            wq::DecodeClass c{};
+            c.lpr = lpr;
+            c.gpl = gpl;
+            cls.push_back(c);
+            members.emplace_back();
+            work.push_back(0.0);
         }
+        const int r = rows_per_step(lpr, gpl);
+        e.steps = (e.n + r - 1) / r;
+        e.first_step = cls[ci].steps;
+        cls[ci].steps += e.steps;
+        members[ci].push_back(i);
+        work[ci] += (double)l.N * (double)(l.K / 2 + l.K / 16);
     }
-    if (chain) {
-        // More than two conflicts somewhere: order every linear after its
-        // predecessor, which orders it after all earlier ones.
-        for (int i = 0; i < count; ++i) {
-            ents[i].dep0 = i - 1;
-            ents[i].dep1 = -1;
-        }
+    const int capacity = max_gpl <= 4 ? capacity4 : capacity8;
+    double total = 0.0;
+    for (double w : work) total += w;
+    int waves = 0, off = 0;
+    for (size_t c = 0; c < cls.size(); ++c) {
+        int64_t wc = (int64_t)(capacity * work[c] / total);
+        wc = std::max<int64_t>(1, std::min<int64_t>(wc, cls[c].steps));
+        cls[c].waves_begin = waves;
+        cls[c].waves = (int32_t)wc;
+        waves += (int)wc;
+        cls[c].first = off;
+        cls[c].count = (int32_t)members[c].size();
+        off += cls[c].count;
     }
-    for (int i = 0; i < count; ++i) {
-        if (ents[i].dep0 >= 0) ents[ents[i].dep0].signal = 1;
-        if (ents[i].dep1 >= 0) ents[ents[i].dep1].signal = 1;
-    }
-    int64_t tiles_total = 0;
-    for (int i = 0; i < count; ++i) {
-        wq::DecodeEntry& e = ents[i];
-        const int64_t k = (int64_t)e.ng * 32;
-        const int u = rows_per_step(e.gpl);
-        const int64_t step_bytes = (int64_t)u * (k / 2 + 2 * e.ng);
-        const bool chained = e.signal || e.dep0 >= 0 || e.dep1 >= 0;
-        const int64_t target = chained ? kTileBytesChained : kTileBytesFree;
-        const int64_t steps = std::max<int64_t>(1, (target + step_bytes / 2) / step_bytes);
-        const int64_t rows = std::min<int64_t>(steps * u, ((e.n + u - 1) / u) * u);
-        e.tile_rows = (int32_t)rows;
-        e.tiles = (int32_t)((e.n + rows - 1) / rows);
-        e.first_tile = (int32_t)tiles_total;
-        tiles_total += e.tiles;
-        if (tiles_total > 0x7fffffff) return false;
-    }
-    total_tiles = (int)tiles_total;
-    return true;
+    GroupPlan gp;
+    gp.nclasses = (int)cls.size();
+    gp.max_gpl = max_gpl;
+    gp.waves = waves;
+    gp.off_entries = align16(bytes.size());
+    gp.off_classes = align16(gp.off_entries + sizeof(wq::DecodeEntry) * count);
+    gp.off_list = align16(gp.off_classes + sizeof(wq::DecodeClass) * cls.size());
+    bytes.resize(align16(gp.off_list + sizeof(int32_t) * count), 0);
+    std::memcpy(bytes.data() + gp.off_entries, ents.data(), sizeof(wq::DecodeEntry) * count);
+    std::memcpy(bytes.data() + gp.off_classes, cls.data(), sizeof(wq::DecodeClass) * cls.size());
+    int32_t* list = reinterpret_cast<int32_t*>(bytes.data() + gp.off_list);
+    for (size_t c = 0; c < cls.size(); ++c)
+        for (size_t m = 0; m < members[c].size(); ++m) list[cls[c].first + m] = members[c][m];
+    return gp;
 }
 
-wq_status get_workspace(const char* fn, hipStream_t stream, int count, DecodeWorkspace*& out) {
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
+// Per (device, stream) workspace: the device copy of the last plan, a pinned
+// staging buffer for uploads, and the device's resident-wave capacity.
+// Allocated on first use and kept until the process ends.
+struct DecodeWorkspace {
+    unsigned char* d_plan = nullptr;
+    unsigned char* h_stage = nullptr;
+    size_t capacity = 0;                 // bytes of d_plan and h_stage
+    hipEvent_t staged = nullptr;         // the last upload has been read by the device
+    bool stage_pending = false;
+    std::vector<unsigned char> uploaded; // bytes of the plan now in d_plan
+    int waves4 = 0, waves8 = 0;          // resident waves of the two kernel variants
+};
+
+std::mutex g_ws_mu;
+std::map<std::pair<int, hipStream_t>, DecodeWorkspace*> g_ws;
+
+wq_status get_workspace(const char* fn, hipStream_t stream, DecodeWorkspace*& out) {
+    int device = 0;
+    hipError_t e = hipGetDevice(&device);
     if (e != hipSuccess) return hip_status(fn, e);
-    DecodeWorkspace*& ws = g_ws[std::make_pair(dev, stream)];
+    DecodeWorkspace*& ws = g_ws[std::make_pair(device, stream)];
     if (!ws) {
-        ws = new DecodeWorkspace();
-        int cus = 0;
-        if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess)
-            return hip_status(fn, e);
-        ws->blocks = std::max(1, cus) * 2;  // 8 waves per CU
-        if (const char* env = std::getenv("WQ_DECODE_SPIN_LIMIT")) ws->spin_limit = (uint32_t)std::strtoul(env, nullptr, 10);
-        if ((e = hipEventCreateWithFlags(&ws->staged, hipEventDisableTiming)) != hipSuccess) return hip_status(fn, e);
-    }
-    if (count > ws->capacity) {
-        // Growing: make sure no launch still uses the old buffers.
-        if (ws->d_table || ws->stage_pending) {
-            if ((e = hipStreamSynchronize(stream)) != hipSuccess) return hip_status(fn, e);
-            ws->stage_pending = false;
-        }
-        if (ws->d_table) (void)hipFree(ws->d_table);
-        if (ws->d_sync) (void)hipFree(ws->d_sync);
-        if (ws->h_stage) (void)hipHostFree(ws->h_stage);
-        ws->d_table = nullptr;
-        ws->d_sync = nullptr;
-        ws->h_stage = nullptr;
-        ws->uploaded.clear();
-        int cap = 64;
-        while (cap < count) cap *= 2;
-        if ((e = hipMalloc(reinterpret_cast<void**>(&ws->d_table), sizeof(wq::DecodeEntry) * cap)) != hipSuccess)
-            return hip_status(fn, e);
-        if ((e = hipMalloc(reinterpret_cast<void**>(&ws->d_sync), sizeof(uint32_t) * (wq::kSyncHeader + cap))) != hipSuccess)
-            return hip_status(fn, e);
-        if ((e = hipMemset(ws->d_sync, 0, sizeof(uint32_t) * (wq::kSyncHeader + cap))) != hipSuccess)
-            return hip_status(fn, e);
-        if ((e = hipHostMalloc(reinterpret_cast<void**>(&ws->h_stage), sizeof(wq::DecodeEntry) * cap)) != hipSuccess)
-            return hip_status(fn, e);
-        ws->capacity = cap;
+        std::unique_ptr<DecodeWorkspace> fresh(new DecodeWorkspace());
+        if ((e = hipEventCreateWithFlags(&fresh->staged, hipEventDisableTiming)) != hipSuccess) return hip_status(fn, e);
+        if ((e = wq::grouped_capacity(4, device, fresh->waves4)) != hipSuccess) return hip_status(fn, e);
+        if ((e = wq::grouped_capacity(8, device, fresh->waves8)) != hipSuccess) return hip_status(fn, e);
+        ws = fresh.release();
     }
     out = ws;
     return WQ_OK;
 }
 
-// Run the linears with the persistent kernel (M = 1, K <= 16384).
-wq_status decode_persistent(const char* fn, const std::vector<wq_linear>& lin, hipStream_t stream) {
-    std::vector<wq::DecodeEntry> ents;
-    int total_tiles = 0, max_gpl = 1;
-    if (!plan_decode(lin, ents, total_tiles, max_gpl)) {
-        for (const wq_linear& l : lin) {
-            const wq_status st = hip_status(fn, wq::launch_gemv(l.packed_w, l.scales, l.x, l.y, l.N, l.K, 1, stream));
-            if (st != WQ_OK) return st;
-        }
-        return WQ_OK;
+// Make sure d_plan holds `bytes` (uploading only when it changed).
+wq_status upload_plan(const char* fn, DecodeWorkspace* ws, std::vector<unsigned char>& bytes, hipStream_t stream) {
+    if (ws->uploaded == bytes) return WQ_OK;
+    hipError_t e;
+    if (bytes.size() > ws->capacity) {
+        // Growing: make sure no launch or copy still uses the old buffers.
+        if (ws->d_plan && (e = hipStreamSynchronize(stream)) != hipSuccess) return hip_status(fn, e);
+        if (ws->d_plan) (void)hipFree(ws->d_plan);
+        if (ws->h_stage) (void)hipHostFree(ws->h_stage);
+        ws->d_plan = nullptr;
+        ws->h_stage = nullptr;
+        ws->stage_pending = false;
+        ws->uploaded.clear();
+        size_t cap = 4096;
+        while (cap < bytes.size()) cap *= 2;
+        if ((e = hipMalloc(reinterpret_cast<void**>(&ws->d_plan), cap)) != hipSuccess) return hip_status(fn, e);
+        if ((e = hipHostMalloc(reinterpret_cast<void**>(&ws->h_stage), cap)) != hipSuccess) return hip_status(fn, e);
+        ws->capacity = cap;
     }
-    const int count = (int)lin.size();
+    if (ws->stage_pending && (e = hipEventSynchronize(ws->staged)) != hipSuccess) return hip_status(fn, e);
+    std::memcpy(ws->h_stage, bytes.data(), bytes.size());
+    if ((e = hipMemcpyAsync(ws->d_plan, ws->h_stage, bytes.size(), hipMemcpyHostToDevice, stream)) != hipSuccess)
+        return hip_status(fn, e);
+    if ((e = hipEventRecord(ws->staged, stream)) != hipSuccess) return hip_status(fn, e);
+    ws->stage_pending = true;
+    ws->uploaded.swap(bytes);
+    return WQ_OK;
+}
+
+wq_status decode_per_linear(const char* fn, const wq_linear* lin, int64_t count, int64_t m, hipStream_t stream) {
+    for (int64_t i = 0; i < count; ++i) {
+        const wq_linear& l = lin[i];
+        const wq_status st = hip_status(fn, wq::launch_gemv(l.packed_w, l.scales, l.x, l.y, l.N, l.K, m, stream));
+        if (st != WQ_OK) return st;
+    }
+    return WQ_OK;
+}
+
+// M = 1: one grouped launch per dependency group (one GEMV launch for
+// linears with K > 16384), all on `stream`.
+wq_status decode_grouped(const char* fn, const std::vector<wq_linear>& lin, hipStream_t stream) {
+    const std::vector<Group> groups = split_groups(lin);
     std::lock_guard<std::mutex> guard(g_ws_mu);
     DecodeWorkspace* ws = nullptr;
-    wq_status st = get_workspace(fn, stream, count, ws);
+    wq_status st = get_workspace(fn, stream, ws);
     if (st != WQ_OK) return st;
-    hipError_t e;
-    const size_t bytes = sizeof(wq::DecodeEntry) * count;
-    if (ws->uploaded.size() != ents.size() || std::memcmp(ws->uploaded.data(), ents.data(), bytes) != 0) {
-        if (ws->stage_pending && (e = hipEventSynchronize(ws->staged)) != hipSuccess) return hip_status(fn, e);
-        std::memcpy(ws->h_stage, ents.data(), bytes);
-        if ((e = hipMemcpyAsync(ws->d_table, ws->h_stage, bytes, hipMemcpyHostToDevice, stream)) != hipSuccess)
-            return hip_status(fn, e);
-        if ((e = hipEventRecord(ws->staged, stream)) != hipSuccess) return hip_status(fn, e);
-        ws->stage_pending = true;
-        ws->uploaded = ents;
+    std::vector<unsigned char> bytes;
+    std::vector<GroupPlan> plans(groups.size());
+    for (size_t i = 0; i < groups.size(); ++i)
+        if (groups[i].grouped) plans[i] = plan_group(lin, groups[i], ws->waves4, ws->waves8, bytes);
+    if (!bytes.empty() && (st = upload_plan(fn, ws, bytes, stream)) != WQ_OK) return st;
+    for (size_t i = 0; i < groups.size(); ++i) {
+        const Group& g = groups[i];
+        if (!g.grouped) {
+            if ((st = decode_per_linear(fn, &lin[g.begin], g.end - g.begin, 1, stream)) != WQ_OK) return st;
+            continue;
+        }
+        const GroupPlan& gp = plans[i];
+        wq::DecodePlan p;
+        p.entries = reinterpret_cast<const wq::DecodeEntry*>(ws->d_plan + gp.off_entries);
+        p.classes = reinterpret_cast<const wq::DecodeClass*>(ws->d_plan + gp.off_classes);
+        p.class_lin = reinterpret_cast<const int32_t*>(ws->d_plan + gp.off_list);
+        p.nclasses = gp.nclasses;
+        if ((st = hip_status(fn, wq::launch_grouped_m1(p, gp.max_gpl, gp.waves, stream))) != WQ_OK) return st;
     }
-    return hip_status(fn, wq::launch_decode_m1(ws->d_table, count, total_tiles, max_gpl, ws->d_sync,
-                                               ws->spin_limit, ws->blocks, stream));
+    return WQ_OK;
 }
 }  // namespace
 
@@ -331,17 +419,9 @@ wq_status wq_decode_linears(const wq_linear* linears, int64_t count, int64_t M, 
     }
     (void)hipGetLastError();
     const hipStream_t s = static_cast<hipStream_t>(stream);
-    bool persistent = (M == 1);
-    for (int64_t i = 0; i < count && persistent; ++i)
-        persistent = (lin[i].K / 32 + 63) / 64 <= wq::kDecodeMaxGpl && lin[i].N <= 0x7fffffff;
-    if (persistent) return decode_persistent(fn, lin, s);
-    // Other shapes: one launch per linear, in stream order.
-    for (int64_t i = 0; i < count; ++i) {
-        const wq_linear& l = lin[i];
-        const wq_status st = hip_status(fn, wq::launch_gemv(l.packed_w, l.scales, l.x, l.y, l.N, l.K, M, s));
-        if (st != WQ_OK) return st;
-    }
-    return WQ_OK;
+    if (M == 1) return decode_grouped(fn, lin, s);
+    // Batches: one launch per linear, in stream order.
+    return decode_per_linear(fn, lin.data(), count, M, s);
 }
 
 }  // extern "C"

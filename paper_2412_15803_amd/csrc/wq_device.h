@@ -20,11 +20,26 @@ namespace wq {
 namespace dev {
 
 typedef _Float16 half2v __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));  // one 16-byte load
 
 constexpr int kGroup = 32;
 constexpr int kWave = 64;
 
 __device__ __forceinline__ half2v as_h2(uint32_t v) { return __builtin_bit_cast(half2v, v); }
+
+// Global-address-space views of device pointers.  Pointers read from a table
+// are generic to the compiler, which would otherwise emit FLAT accesses; those
+// count on the scalar-memory counter too, so every wait for a table read
+// would also wait for all weight loads in flight.
+#define WQ_GLOBAL __attribute__((address_space(1)))
+template <typename T>
+__device__ __forceinline__ const WQ_GLOBAL T* gbl(const T* p) {
+    return (const WQ_GLOBAL T*)p;
+}
+template <typename T>
+__device__ __forceinline__ WQ_GLOBAL T* gbl(T* p) {
+    return (WQ_GLOBAL T*)p;
+}
 
 // x for one group (32 fp16) as 16 half2 pairs, per word c ordered
 // (x[8c+0], x[8c+4]), (x[8c+1], x[8c+5]), (x[8c+2], x[8c+6]), (x[8c+3], x[8c+7]):
@@ -34,10 +49,10 @@ __device__ __forceinline__ half2v as_h2(uint32_t v) { return __builtin_bit_cast(
 // and 16 * (3, 7).  OR-ing 0x6400 into a half makes the fp16 value 1024 + v,
 // and (1024 + q) - 1032 = q - 8 = (1024 + 16 q) / 16 - 72 exactly.
 __device__ __forceinline__ void load_x_group(const uint16_t* __restrict__ xg, half2v out[16]) {
-    const uint4* src = reinterpret_cast<const uint4*>(xg);
+    const WQ_GLOBAL u32x4* src = gbl(reinterpret_cast<const u32x4*>(xg));
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-        const uint4 d = src[c];
+        const u32x4 d = src[c];
         out[4 * c + 0] = as_h2((d.x & 0xFFFFu) | (d.z << 16));
         out[4 * c + 1] = as_h2((d.x >> 16) | (d.z & 0xFFFF0000u));
         out[4 * c + 2] = as_h2((d.y & 0xFFFFu) | (d.w << 16));
@@ -45,15 +60,23 @@ __device__ __forceinline__ void load_x_group(const uint16_t* __restrict__ xg, ha
     }
 }
 
+// (w & mask) | magic in one VALU op.  The constants live in registers
+// (loop-invariant), which the three-operand form needs on this target.
+__device__ __forceinline__ uint32_t and_or(uint32_t w, uint32_t mask, uint32_t magic) {
+    uint32_t r;
+    asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(w), "v"(mask), "v"(magic));
+    return r;
+}
+
 __device__ __forceinline__ float dot_word(uint32_t w, const half2v* xp, float acc) {
     const half2v k1032 = {(_Float16)1032.0f, (_Float16)1032.0f};
     const half2v k1_16 = {(_Float16)0.0625f, (_Float16)0.0625f};
     const half2v km72 = {(_Float16)-72.0f, (_Float16)-72.0f};
     const uint32_t w8 = w >> 8;
-    const half2v q04 = as_h2((w & 0x000F000Fu) | 0x64006400u) - k1032;
-    const half2v q15 = as_h2((w & 0x00F000F0u) | 0x64006400u) * k1_16 + km72;
-    const half2v q26 = as_h2((w8 & 0x000F000Fu) | 0x64006400u) - k1032;
-    const half2v q37 = as_h2((w8 & 0x00F000F0u) | 0x64006400u) * k1_16 + km72;
+    const half2v q04 = as_h2(and_or(w, 0x000F000Fu, 0x64006400u)) - k1032;
+    const half2v q15 = as_h2(and_or(w, 0x00F000F0u, 0x64006400u)) * k1_16 + km72;
+    const half2v q26 = as_h2(and_or(w8, 0x000F000Fu, 0x64006400u)) - k1032;
+    const half2v q37 = as_h2(and_or(w8, 0x00F000F0u, 0x64006400u)) * k1_16 + km72;
     acc = __builtin_amdgcn_fdot2(q04, xp[0], acc, false);
     acc = __builtin_amdgcn_fdot2(q15, xp[1], acc, false);
     acc = __builtin_amdgcn_fdot2(q26, xp[2], acc, false);
@@ -62,7 +85,7 @@ __device__ __forceinline__ float dot_word(uint32_t w, const half2v* xp, float ac
 }
 
 // sum_{k in group} (q_k - 8) * x_k for one 16-byte group of codes.
-__device__ __forceinline__ float dot_group(const uint4 wv, const half2v xg[16]) {
+__device__ __forceinline__ float dot_group(const u32x4 wv, const half2v xg[16]) {
     float a0 = dot_word(wv.x, xg + 0, 0.0f);
     float a1 = dot_word(wv.y, xg + 4, 0.0f);
     a0 = dot_word(wv.z, xg + 8, a0);
@@ -76,67 +99,87 @@ __device__ __forceinline__ float dpp_add(float v) {
     return v + __builtin_bit_cast(float, t);
 }
 
-// Sum over the 64 lanes of a wave; the total lands in lane 63.
-__device__ __forceinline__ float wave_sum_to_last_lane(float v) {
+// Sum over each aligned segment of LPR lanes (16, 32 or 64); the segment's
+// total lands in its last lane.
+template <int LPR>
+__device__ __forceinline__ float segment_sum(float v) {
     v = dpp_add<0xB1, 0xF>(v);   // quad_perm [1,0,3,2]
     v = dpp_add<0x4E, 0xF>(v);   // quad_perm [2,3,0,1]
     v = dpp_add<0x141, 0xF>(v);  // row_half_mirror: 8-lane sums
-    v = dpp_add<0x140, 0xF>(v);  // row_mirror: 16-lane sums
-    v = dpp_add<0x142, 0xA>(v);  // row_bcast:15 into rows 1, 3
-    v = dpp_add<0x143, 0xC>(v);  // row_bcast:31 into rows 2, 3
+    v = dpp_add<0x140, 0xF>(v);  // row_mirror: 16-lane sums in every lane of a row
+    if constexpr (LPR >= 32) v = dpp_add<0x142, 0xA>(v);  // row_bcast:15 into rows 1, 3
+    if constexpr (LPR >= 64) v = dpp_add<0x143, 0xC>(v);  // row_bcast:31 into rows 2, 3
     return v;
 }
 
 // ------------------------------------------------------- batch-1 row steps
 //
-// A "step" is U consecutive rows of one linear.  Lane l owns groups
-// l, l + 64, ..., l + 64 (GPL - 1) of every row, so each wave-wide 16-byte
-// load covers 1 KiB of one row contiguously.  A step holds U * GPL <= 8
-// loads per lane.
-template <int GPL>
+// A wave is split into 64/LPR slots of LPR lanes; each slot works on its own
+// row.  Lane `sub` of a slot owns groups sub, sub + LPR, ...,
+// sub + LPR (GPL - 1) of that row, so one wave-wide 16-byte load reads LPR x
+// 16 contiguous bytes of each slot's row.  LPR is chosen per shape so that
+// LPR * GPL covers the row's groups with no idle lanes where possible.
+//
+// A "step" is U rows per slot (U * 64/LPR rows per wave) and U * GPL <= 8
+// loads per lane; slot s takes rows row0 + s*U .. row0 + s*U + U - 1.
+template <int LPR, int GPL>
 struct StepShape {
-    static constexpr int U = GPL >= 8 ? 1 : 8 / GPL;  // rows per step
+    static constexpr int SLOTS = kWave / LPR;
+    static constexpr int U = GPL >= 8 ? 1 : 8 / GPL;  // rows per slot
+    static constexpr int ROWS = U * SLOTS;            // rows per step
 };
 
 struct StepBuf {
-    uint4 w[8];
+    u32x4 w[8];
     uint32_t s[8];
 };
 
-// x groups of this lane for one linear.  Lanes whose group index runs past
-// the row get zeros and a disabled flag.
-template <int GPL, int MAXG>
-__device__ __forceinline__ void load_x_lane(const uint16_t* __restrict__ x, int ng, int lane,
-                                            half2v (&xr)[MAXG][16], bool (&act)[MAXG]) {
+// x groups of this lane: every group's loads are issued before any is
+// rearranged, so they share one round trip.  Lanes whose group index runs
+// past the row get zeros.
+template <int LPR, int GPL, int MAXG>
+__device__ __forceinline__ void load_x_lane(const uint16_t* x, int ng, int lane, half2v (&xr)[MAXG][16]) {
+    const int sub = lane & (LPR - 1);
+    u32x4 raw[GPL][4];
 #pragma unroll
     for (int j = 0; j < GPL; ++j) {
-        const int g = lane + kWave * j;
-        act[j] = g < ng;
-        const int gc = act[j] ? g : ng - 1;
-        load_x_group(x + (int64_t)gc * kGroup, xr[j]);
-        if (!act[j]) {
+        const WQ_GLOBAL u32x4* src = gbl(reinterpret_cast<const u32x4*>(x + (int64_t)min(sub + LPR * j, ng - 1) * kGroup));
 #pragma unroll
-            for (int p = 0; p < 16; ++p) xr[j][p] = half2v{(_Float16)0.0f, (_Float16)0.0f};
+        for (int c = 0; c < 4; ++c) raw[j][c] = src[c];
+    }
+#pragma unroll
+    for (int j = 0; j < GPL; ++j) {
+        const bool act = sub + LPR * j < ng;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const u32x4 d = raw[j][c];
+            xr[j][4 * c + 0] = as_h2(act ? (d.x & 0xFFFFu) | (d.z << 16) : 0u);
+            xr[j][4 * c + 1] = as_h2(act ? (d.x >> 16) | (d.z & 0xFFFF0000u) : 0u);
+            xr[j][4 * c + 2] = as_h2(act ? (d.y & 0xFFFFu) | (d.w << 16) : 0u);
+            xr[j][4 * c + 3] = as_h2(act ? (d.y >> 16) | (d.w & 0xFFFF0000u) : 0u);
         }
     }
 }
 
-// Issue the loads of rows [row0, row0 + U) (clamped to last_row, so every
+// Issue the loads of rows [row0, row0 + ROWS) (clamped to last_row, so every
 // lane always loads a valid address and no branch is needed).
-template <int GPL>
-__device__ __forceinline__ void issue_step(StepBuf& b, const uint4* packed,
-                                           const uint16_t* scales, int64_t row0,
-                                           int64_t last_row, int ng, int lane) {
-    constexpr int U = StepShape<GPL>::U;
+template <int LPR, int GPL>
+__device__ __forceinline__ void issue_step(StepBuf& b, const u32x4* packed, const uint16_t* scales,
+                                           int64_t row0, int64_t last_row, int ng, int lane) {
+    using S = StepShape<LPR, GPL>;
+    const int slot = lane / LPR;
+    const int sub = lane & (LPR - 1);
+    const WQ_GLOBAL u32x4* gp = gbl(packed);
+    const WQ_GLOBAL uint16_t* gs = gbl(scales);
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-        const int64_t r = min(row0 + u, last_row);
+    for (int u = 0; u < S::U; ++u) {
+        const int64_t r = min(row0 + slot * S::U + u, last_row);
 #pragma unroll
         for (int j = 0; j < GPL; ++j) {
-            const int g = min(lane + kWave * j, ng - 1);
+            const int g = min(sub + LPR * j, ng - 1);
             const int64_t idx = r * ng + g;
-            b.w[u * GPL + j] = packed[idx];
-            b.s[u * GPL + j] = scales[idx];
+            b.w[u * GPL + j] = gp[idx];
+            b.s[u * GPL + j] = gs[idx];
         }
     }
     // Keep this step's loads ahead of anything issued later: the load counter
@@ -148,24 +191,37 @@ __device__ __forceinline__ void issue_step(StepBuf& b, const uint4* packed,
     __builtin_amdgcn_sched_barrier(0);
 }
 
-// Dot products, wave reduction and fp16 store of the rows of one step;
-// only rows below row0 + nrows are written.
-template <int GPL, int MAXG>
+// Dot products, segment reduction and fp16 store of one step; only rows
+// below row0 + nrows are written.  Lanes past the row's groups hold zero x,
+// so their (clamped, finite) codes contribute nothing.
+template <int LPR, int GPL, int MAXG>
 __device__ __forceinline__ void compute_step(const StepBuf& b, const half2v (&xr)[MAXG][16],
-                                             const bool (&act)[MAXG], uint16_t* __restrict__ y,
-                                             int64_t row0, int nrows, int lane) {
-    constexpr int U = StepShape<GPL>::U;
+                                             uint16_t* __restrict__ y, int64_t row0, int nrows, int lane) {
+    using S = StepShape<LPR, GPL>;
+    const int slot = lane / LPR;
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
+    for (int u = 0; u < S::U; ++u) {
         float acc = 0.0f;
 #pragma unroll
         for (int j = 0; j < GPL; ++j) {
-            const float s = act[j] ? __half2float(__ushort_as_half((uint16_t)b.s[u * GPL + j])) : 0.0f;
+            const float s = __half2float(__ushort_as_half((uint16_t)b.s[u * GPL + j]));
             acc = fmaf(s, dot_group(b.w[u * GPL + j], xr[j]), acc);
         }
-        const float tot = wave_sum_to_last_lane(acc);
-        if (lane == kWave - 1 && u < nrows) y[row0 + u] = __half_as_ushort(__float2half_rn(tot));
+        const float tot = segment_sum<LPR>(acc);
+        const int rr = slot * S::U + u;
+        if ((lane & (LPR - 1)) == LPR - 1 && rr < nrows) gbl(y)[row0 + rr] = __half_as_ushort(__float2half_rn(tot));
     }
+}
+
+// Lanes per row and groups per lane for a row of ng groups (ng <= 512):
+// an exact cover when one exists, else 64 lanes with the tail lanes idle.
+__host__ __device__ inline void pick_shape(int ng, int& lpr, int& gpl) {
+    if (ng <= 16) { lpr = 16; gpl = 1; return; }
+    if (ng % 64 == 0) { lpr = 64; gpl = ng / 64; return; }
+    if (ng % 32 == 0 && (ng / 32) % 2 == 1 && ng / 32 <= 7) { lpr = 32; gpl = ng / 32; return; }
+    if (ng % 16 == 0 && (ng / 16) % 2 == 1 && ng / 16 <= 7) { lpr = 16; gpl = ng / 16; return; }
+    lpr = 64;
+    gpl = (ng + 63) / 64;
 }
 
 }  // namespace dev

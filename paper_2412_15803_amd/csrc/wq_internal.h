@@ -16,36 +16,54 @@ hipError_t launch_gemv(const uint32_t* packed, const uint16_t* scales,
                        const uint16_t* x, uint16_t* y,
                        int64_t n, int64_t k, int64_t m, hipStream_t stream);
 
-// One linear of a decode step as the persistent decode kernel sees it
-// (built on the host, uploaded once per distinct descriptor list).
+// One linear of a grouped launch as the kernel sees it (built on the host,
+// uploaded once per distinct descriptor list).
 struct DecodeEntry {
     const void* packed;      // [n][ng] 16-byte groups
     const uint16_t* scales;  // [n][ng]
     const uint16_t* x;       // [ng * 32]
     uint16_t* y;             // [n]
     int64_t n;
+    int64_t first_step;      // first step of this linear in its class's numbering
+    int64_t steps;           // steps of this linear: ceil(n / rows per step)
     int32_t ng;              // groups of 32 per row
-    int32_t gpl;             // groups per lane: ceil(ng / 64)
-    int32_t tile_rows;       // rows per claimed tile (a multiple of the step height)
-    int32_t tiles;           // ceil(n / tile_rows)
-    int32_t first_tile;      // global index of this linear's first tile
-    int32_t dep0, dep1;      // linears that must complete before this one reads x (-1: none)
-    int32_t signal;          // nonzero if a later linear waits for this one
-    int32_t pad[2];
+    int32_t lpr;             // lanes per row (16, 32 or 64)
+    int32_t gpl;             // groups per lane (lpr * gpl >= ng)
+    int32_t pad;
 };
-static_assert(sizeof(DecodeEntry) == 80, "DecodeEntry layout");
+static_assert(sizeof(DecodeEntry) == 72, "DecodeEntry layout");
 
-// Counter words of the decode workspace: ticket, exit count, error flag,
-// reserved, then one completed-tile counter per linear.
-constexpr int kSyncHeader = 4;
+// Linears of one launch with the same step shape.  The class's steps are
+// split into `waves` equal contiguous ranges, one per wave, for the waves
+// [waves_begin, waves_begin + waves) of the grid.
+struct DecodeClass {
+    int32_t lpr, gpl;     // the class's step shape
+    int32_t first;        // offset of its linears in the class list
+    int32_t count;        // number of linears
+    int64_t steps;        // steps over all its linears
+    int32_t waves_begin;
+    int32_t waves;
+};
+static_assert(sizeof(DecodeClass) == 32, "DecodeClass layout");
 
-// Largest groups-per-lane the persistent decode kernel handles (K <= 16384).
+// Device-side view of one grouped launch: the entries, the class
+// descriptors and, per class, the indices of its linears in order.
+struct DecodePlan {
+    const DecodeEntry* entries;
+    const DecodeClass* classes;
+    const int32_t* class_lin;
+    int32_t nclasses;
+};
+
+// Largest groups-per-lane of the grouped kernel (K <= 16384).
 constexpr int kDecodeMaxGpl = 8;
+constexpr int kMaxClasses = 16;
 
-// Launch the persistent decode-step kernel over `count` entries already in
-// device memory.  `sync` must hold kSyncHeader + count zeroed words; the
-// kernel leaves them zeroed again when it finishes.
-hipError_t launch_decode_m1(const DecodeEntry* table, int count, int total_tiles, int max_gpl,
-                            uint32_t* sync, uint32_t spin_limit, int blocks, hipStream_t stream);
+// Launch the grouped batch-1 GEMV over a plan in device memory with `waves`
+// waves (the sum of the classes' waves).
+hipError_t launch_grouped_m1(const DecodePlan& plan, int max_gpl, int waves, hipStream_t stream);
+
+// Waves of the grouped kernel (for max_gpl) that the device holds at once.
+hipError_t grouped_capacity(int max_gpl, int device, int& waves);
 
 }  // namespace wq

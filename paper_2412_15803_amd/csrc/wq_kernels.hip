@@ -61,43 +61,43 @@ __global__ __launch_bounds__(kBlock) void pack_kernel(const float* __restrict__ 
 
 // ------------------------------------------------------------ batch-1 GEMV
 //
-// Each wave owns a contiguous block of rows and walks it in steps of U rows
-// through two register buffers: compute buffer A, refill A with the step two
-// ahead, compute B, refill B.  Whenever the wave waits for a buffer, the other
+// Each wave owns a contiguous block of rows and walks it in steps through two
+// register buffers: compute buffer A, refill A with the step two ahead,
+// compute B, refill B.  Whenever the wave waits for a buffer, the other
 // buffer's loads are still in flight.
-template <int GPL>
-__global__ __launch_bounds__(kBlock) void gemv_m1_kernel(const uint4* packed,
-                                                         const uint16_t* scales,
+template <int LPR, int GPL>
+__global__ __launch_bounds__(kBlock) void gemv_m1_kernel(const u32x4* packed, const uint16_t* scales,
                                                          const uint16_t* __restrict__ x,
                                                          uint16_t* __restrict__ y, int64_t n, int ng,
                                                          int64_t rows_per_wave) {
-    constexpr int U = StepShape<GPL>::U;
+    constexpr int R = StepShape<LPR, GPL>::ROWS;
     const int lane = threadIdx.x & (kWave - 1);
-    const int64_t wave = (int64_t)blockIdx.x * kWavesPerBlock + threadIdx.x / kWave;
+    // Wave-uniform (the compiler cannot see that threadIdx.x / 64 is), so
+    // the row bookkeeping stays in scalar registers and branches uniform.
+    const int64_t wave = (int64_t)__builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerBlock + threadIdx.x / kWave);
     const int64_t rb = wave * rows_per_wave;
     if (rb >= n) return;
     const int64_t re = min(n, rb + rows_per_wave);
     const int64_t last = re - 1;
-    const int64_t steps = (re - rb + U - 1) / U;
+    const int64_t steps = (re - rb + R - 1) / R;
 
     half2v xr[GPL][16];
-    bool act[GPL];
-    load_x_lane<GPL, GPL>(x, ng, lane, xr, act);
+    load_x_lane<LPR, GPL, GPL>(x, ng, lane, xr);
 
-    // Two register buffers; the loop starts two steps early so that the first
-    // pass only issues, and every load of the kernel comes from the same two
-    // issue sites (one register assignment, no prologue copies that would
-    // force a full wait).  Loads past the wave's rows are clamped to its last
-    // row, so every issue is unconditional and the wait counts stay exact.
+    // The loop starts two steps early so that the first pass only issues and
+    // every load comes from the same two issue sites (one register
+    // assignment, no prologue copies that would force a full wait).  Loads
+    // past the wave's rows are clamped to its last row, so every issue is
+    // unconditional and the wait counts stay exact.
     StepBuf a, b;
     for (int64_t s = -2; s < steps; s += 2) {
-        const int64_t ra = rb + s * U;
-        if (s >= 0) compute_step<GPL, GPL>(a, xr, act, y, ra, (int)min((int64_t)U, re - ra), lane);
-        issue_step<GPL>(a, packed, scales, ra + 2 * U, last, ng, lane);
-        const int64_t rbb = ra + U;
+        const int64_t ra = rb + s * R;
+        if (s >= 0) compute_step<LPR, GPL, GPL>(a, xr, y, ra, (int)min((int64_t)R, re - ra), lane);
+        issue_step<LPR, GPL>(a, packed, scales, ra + 2 * R, last, ng, lane);
+        const int64_t rbb = ra + R;
         if (s + 1 >= 0 && s + 1 < steps)
-            compute_step<GPL, GPL>(b, xr, act, y, rbb, (int)min((int64_t)U, re - rbb), lane);
-        issue_step<GPL>(b, packed, scales, rbb + 2 * U, last, ng, lane);
+            compute_step<LPR, GPL, GPL>(b, xr, y, rbb, (int)min((int64_t)R, re - rbb), lane);
+        issue_step<LPR, GPL>(b, packed, scales, rbb + 2 * R, last, ng, lane);
     }
 }
 
@@ -107,7 +107,7 @@ __global__ __launch_bounds__(kBlock) void gemv_m1_kernel(const uint4* packed,
 // over the row's groups and read x straight from global memory.  Covers the
 // shapes the tuned kernels do not (M > 1, K > 16384 at M = 1).
 template <int MC>
-__global__ __launch_bounds__(kBlock) void gemv_generic_kernel(const uint4* packed,
+__global__ __launch_bounds__(kBlock) void gemv_generic_kernel(const u32x4* packed,
                                                               const uint16_t* scales,
                                                               const uint16_t* __restrict__ x,
                                                               uint16_t* __restrict__ y, int64_t n,
@@ -125,7 +125,7 @@ __global__ __launch_bounds__(kBlock) void gemv_generic_kernel(const uint4* packe
 #pragma unroll
         for (int i = 0; i < MC; ++i) acc[i] = 0.0f;
         for (int64_t g = lane; g < ng; g += kWave) {
-            const uint4 wv = packed[row * ng + g];
+            const u32x4 wv = packed[row * ng + g];
             const float s = __half2float(__ushort_as_half(scales[row * ng + g]));
 #pragma unroll
             for (int i = 0; i < MC; ++i) {
@@ -138,7 +138,7 @@ __global__ __launch_bounds__(kBlock) void gemv_generic_kernel(const uint4* packe
         }
 #pragma unroll
         for (int i = 0; i < MC; ++i) {
-            const float tot = wave_sum_to_last_lane(acc[i]);
+            const float tot = segment_sum<kWave>(acc[i]);
             if (lane == kWave - 1 && i < mcount) y[(m0 + i) * n + row] = __half_as_ushort(__float2half_rn(tot));
         }
     }
@@ -146,17 +146,17 @@ __global__ __launch_bounds__(kBlock) void gemv_generic_kernel(const uint4* packe
 
 constexpr int kTargetWaves = 256 * 8;  // 256 CUs x 8 waves
 
-template <int GPL>
+template <int LPR, int GPL>
 hipError_t launch_m1(const uint32_t* packed, const uint16_t* scales, const uint16_t* x, uint16_t* y,
                      int64_t n, int64_t ng, hipStream_t stream) {
-    constexpr int U = StepShape<GPL>::U;
-    const int64_t steps = (n + U - 1) / U;
+    constexpr int R = StepShape<LPR, GPL>::ROWS;
+    const int64_t steps = (n + R - 1) / R;
     const int64_t steps_per_wave = (steps + kTargetWaves - 1) / kTargetWaves;
-    const int64_t rows_per_wave = steps_per_wave * U;
+    const int64_t rows_per_wave = steps_per_wave * R;
     const int64_t waves = (n + rows_per_wave - 1) / rows_per_wave;
     const int64_t blocks = (waves + kWavesPerBlock - 1) / kWavesPerBlock;
-    hipLaunchKernelGGL((gemv_m1_kernel<GPL>), dim3((unsigned)blocks), dim3(kBlock), 0, stream,
-                       reinterpret_cast<const uint4*>(packed), scales, x, y, n, (int)ng, rows_per_wave);
+    hipLaunchKernelGGL((gemv_m1_kernel<LPR, GPL>), dim3((unsigned)blocks), dim3(kBlock), 0, stream,
+                       reinterpret_cast<const u32x4*>(packed), scales, x, y, n, (int)ng, rows_per_wave);
     return hipGetLastError();
 }
 
@@ -173,25 +173,23 @@ hipError_t launch_pack(const float* w, uint32_t* packed, uint16_t* scales, int64
 hipError_t launch_gemv(const uint32_t* packed, const uint16_t* scales, const uint16_t* x, uint16_t* y,
                        int64_t n, int64_t k, int64_t m, hipStream_t stream) {
     const int64_t ng = k / kGroup;
-    if (m == 1) {
-        switch ((ng + kWave - 1) / kWave) {
-            case 1: return launch_m1<1>(packed, scales, x, y, n, ng, stream);
-            case 2: return launch_m1<2>(packed, scales, x, y, n, ng, stream);
-            case 3: return launch_m1<3>(packed, scales, x, y, n, ng, stream);
-            case 4: return launch_m1<4>(packed, scales, x, y, n, ng, stream);
-            case 5: return launch_m1<5>(packed, scales, x, y, n, ng, stream);
-            case 6: return launch_m1<6>(packed, scales, x, y, n, ng, stream);
-            case 7: return launch_m1<7>(packed, scales, x, y, n, ng, stream);
-            case 8: return launch_m1<8>(packed, scales, x, y, n, ng, stream);
-            default: break;
-        }
+    if (m == 1 && ng <= 512) {
+        int lpr = 64, gpl = 1;
+        pick_shape((int)ng, lpr, gpl);
+#define WQ_M1_CASE(L, G) \
+    if (lpr == L && gpl == G) return launch_m1<L, G>(packed, scales, x, y, n, ng, stream);
+        WQ_M1_CASE(64, 1) WQ_M1_CASE(64, 2) WQ_M1_CASE(64, 3) WQ_M1_CASE(64, 4)
+        WQ_M1_CASE(64, 5) WQ_M1_CASE(64, 6) WQ_M1_CASE(64, 7) WQ_M1_CASE(64, 8)
+        WQ_M1_CASE(32, 1) WQ_M1_CASE(32, 3) WQ_M1_CASE(32, 5) WQ_M1_CASE(32, 7)
+        WQ_M1_CASE(16, 1) WQ_M1_CASE(16, 3) WQ_M1_CASE(16, 5) WQ_M1_CASE(16, 7)
+#undef WQ_M1_CASE
     }
     constexpr int MC = 4;
     const int64_t mchunks = (m + MC - 1) / MC;
     const int64_t waves = n * mchunks;
     const int64_t blocks = min((waves + kWavesPerBlock - 1) / kWavesPerBlock, (int64_t)1 << 20);
     hipLaunchKernelGGL((gemv_generic_kernel<MC>), dim3((unsigned)blocks), dim3(kBlock), 0, stream,
-                       reinterpret_cast<const uint4*>(packed), scales, x, y, n, ng, m, mchunks);
+                       reinterpret_cast<const u32x4*>(packed), scales, x, y, n, ng, m, mchunks);
     return hipGetLastError();
 }
 
