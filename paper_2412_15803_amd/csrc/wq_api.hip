@@ -190,12 +190,14 @@ GroupPlan plan_group(const std::vector<wq_linear>& lin, const Group& g, int capa
         e.lpr = lpr;
         e.gpl = gpl;
         max_gpl = std::max(max_gpl, gpl);
+        const int sblk = e.ng % 8 == 0 && (reinterpret_cast<uintptr_t>(l.scales) & 15) == 0;
         int ci = 0;
-        while (ci < (int)cls.size() && !(cls[ci].lpr == lpr && cls[ci].gpl == gpl)) ++ci;
+        while (ci < (int)cls.size() && !(cls[ci].lpr == lpr && cls[ci].gpl == gpl && cls[ci].sblk == sblk)) ++ci;
         if (ci == (int)cls.size()) {
             wq::DecodeClass c{};
             c.lpr = lpr;
-            c.gpl = gpl;
+            c.gpl = (int16_t)gpl;
+            c.sblk = (int16_t)sblk;
             cls.push_back(c);
             members.emplace_back();
             work.push_back(0.0);
@@ -263,6 +265,15 @@ wq_status get_workspace(const char* fn, hipStream_t stream, DecodeWorkspace*& ou
         if ((e = hipEventCreateWithFlags(&fresh->staged, hipEventDisableTiming)) != hipSuccess) return hip_status(fn, e);
         if ((e = wq::grouped_capacity(4, device, fresh->waves4)) != hipSuccess) return hip_status(fn, e);
         if ((e = wq::grouped_capacity(8, device, fresh->waves8)) != hipSuccess) return hip_status(fn, e);
+        // Tuning override: fewer waves than the device holds (never more,
+        // since every wave owns a fixed share of the work).
+        if (const char* env = std::getenv("WQ_GROUPED_WAVES")) {
+            const int w = std::atoi(env);
+            if (w > 0) {
+                fresh->waves4 = std::min(fresh->waves4, w);
+                fresh->waves8 = std::min(fresh->waves8, w);
+            }
+        }
         ws = fresh.release();
     }
     out = ws;

@@ -25,39 +25,61 @@ using namespace dev;
 constexpr int kBlock = 256;
 constexpr int kWavesPerBlock = kBlock / kWave;
 
+// One step as the pipeline sees it: everything needed to issue and compute
+// it, so the steady state reads no table entries.
 struct Step {
-    int lin;      // -1 past the end of the wave's range
-    int nrows;    // rows of this step inside its linear
-    int64_t row;  // first row
+    int lin;                 // -1 past the end of the wave's range
+    int nrows;               // rows of this step inside its linear
+    int ng;
+    int64_t row;             // first row
+    const u32x4* packed;
+    const uint16_t* scales;
+    const uint16_t* x;
+    uint16_t* y;
 };
 
 // Walks the wave's step range [pos, end) of a class: steps are numbered per
 // class in linear order, each linear owning steps [first_step, first_step +
-// steps), so the walk only ever moves forward through the class's list.
+// steps), so the walk only ever moves forward through the class's list.  The
+// current linear's fields are cached and reloaded only at a boundary.
 struct StepIter {
-    int idx;       // current position in the class's linear list
-    int lin;       // that linear
-    int64_t pos;   // next step (class numbering)
-    int64_t end;   // one past the wave's last step
+    int idx;        // position in the class's linear list
+    int64_t pos;    // next step (class numbering)
+    int64_t end;    // one past the wave's last step
+    int64_t lin_end;  // first step of the next linear
+    Step cur;       // fields of the current linear (row = its first step's row base)
+    int64_t first_step;
 };
+
+__device__ __forceinline__ void load_linear(StepIter& it, const DecodePlan& p, const DecodeClass& c) {
+    const int lin = p.class_lin[c.first + it.idx];
+    const DecodeEntry& e = p.entries[lin];
+    it.cur.lin = lin;
+    it.cur.ng = e.ng;
+    it.cur.row = e.n;  // rows of the linear, kept here for the clamp
+    it.cur.packed = reinterpret_cast<const u32x4*>(e.packed);
+    it.cur.scales = e.scales;
+    it.cur.x = e.x;
+    it.cur.y = e.y;
+    it.first_step = e.first_step;
+    it.lin_end = e.first_step + e.steps;
+}
 
 template <int R>
 __device__ __forceinline__ Step next_step(StepIter& it, const DecodePlan& p, const DecodeClass& c) {
-    Step s;
+    Step s = it.cur;
     if (it.pos >= it.end) {
         s.lin = -1;
-        s.nrows = 0;
-        s.row = 0;
         return s;
     }
-    while (it.pos >= p.entries[it.lin].first_step + p.entries[it.lin].steps) {
+    while (it.pos >= it.lin_end) {
         ++it.idx;
-        it.lin = p.class_lin[c.first + it.idx];
+        load_linear(it, p, c);
+        s = it.cur;
     }
-    const DecodeEntry& e = p.entries[it.lin];
-    s.lin = it.lin;
-    s.row = (it.pos - e.first_step) * R;
-    s.nrows = (int)min((int64_t)R, e.n - s.row);
+    const int64_t n = it.cur.row;
+    s.row = (it.pos - it.first_step) * R;
+    s.nrows = (int)min((int64_t)R, n - s.row);
     ++it.pos;
     return s;
 }
@@ -72,56 +94,57 @@ struct XSlot {
     int lin;
 };
 
-template <int LPR, int GPL, int MAXG>
-__device__ __forceinline__ void compute_from(const StepBuf& b, XSlot<MAXG>& xs, const Step& s,
-                                             const DecodePlan& p, int lane) {
+template <int LPR, int GPL, int MAXG, bool SBLK>
+__device__ __forceinline__ void compute_from(const StepBuf& b, XSlot<MAXG>& xs, const Step& s, uint16_t* lds,
+                                             int lane) {
     if (s.lin < 0) return;
-    const DecodeEntry& e = p.entries[s.lin];
     if (xs.lin != s.lin) {
-        load_x_lane<LPR, GPL, MAXG>(e.x, e.ng, lane, xs.xr);
+        load_x_lane<LPR, GPL, MAXG>(s.x, s.ng, lane, xs.xr);
         xs.lin = s.lin;
     }
-    compute_step<LPR, GPL, MAXG>(b, xs.xr, e.y, s.row, s.nrows, lane);
+    compute_step<LPR, GPL, MAXG, SBLK>(b, xs.xr, s.y, s.row, s.nrows, s.ng, lds, lane);
 }
 
 // Issues are unconditional: past the end of the range the wave re-loads its
 // last valid step (never computed), so every path through the loop issues
 // the same loads and the compiler's wait counts stay exact.
-template <int LPR, int GPL>
-__device__ __forceinline__ void issue_from(StepBuf& b, const Step& s, const DecodePlan& p, int lane) {
-    const DecodeEntry& e = p.entries[s.lin];
-    issue_step<LPR, GPL>(b, reinterpret_cast<const u32x4*>(e.packed), e.scales, s.row, s.row + s.nrows - 1,
-                         e.ng, lane);
+template <int LPR, int GPL, bool SBLK>
+__device__ __forceinline__ void issue_from(StepBuf& b, const Step& s, int lane) {
+    issue_step<LPR, GPL, SBLK>(b, s.packed, s.scales, s.row, s.row + s.nrows - 1, s.ng, lane);
 }
 
-template <int LPR, int GPL, int MAXG>
+template <int LPR, int GPL, int MAXG, bool SBLK>
 __device__ __forceinline__ void run_range(const DecodePlan& p, const DecodeClass& c, int64_t begin, int64_t end,
-                                          int lane) {
+                                          uint16_t* lds, int lane) {
     constexpr int R = StepShape<LPR, GPL>::ROWS;
     StepIter it;
-    it.idx = 0;
-    it.lin = p.class_lin[c.first];
     it.pos = begin;
     it.end = end;
+    // Find the linear holding step `begin` (scalar binary search would do;
+    // the class lists are short, a forward scan is enough).
+    it.idx = 0;
+    load_linear(it, p, c);
+    while (begin >= it.lin_end) {
+        ++it.idx;
+        load_linear(it, p, c);
+    }
     XSlot<MAXG> xs;
     xs.lin = -1;
     StepBuf a, b;
-    Step sa, sb;
+    Step sa = it.cur, sb = it.cur;
     sa.lin = sb.lin = -1;
-    sa.nrows = sb.nrows = 0;
-    sa.row = sb.row = 0;
     // The first pass only issues; afterwards each pass computes the step a
     // buffer holds and refills that buffer with the wave's next step.
-    Step last;  // the latest valid step (the range is never empty)
+    Step last = it.cur;  // the latest valid step (the range is never empty)
     for (;;) {
-        compute_from<LPR, GPL, MAXG>(a, xs, sa, p, lane);
+        compute_from<LPR, GPL, MAXG, SBLK>(a, xs, sa, lds, lane);
         sa = next_step<R>(it, p, c);
         if (sa.lin >= 0) last = sa;
-        issue_from<LPR, GPL>(a, sa.lin >= 0 ? sa : last, p, lane);
-        compute_from<LPR, GPL, MAXG>(b, xs, sb, p, lane);
+        issue_from<LPR, GPL, SBLK>(a, sa.lin >= 0 ? sa : last, lane);
+        compute_from<LPR, GPL, MAXG, SBLK>(b, xs, sb, lds, lane);
         sb = next_step<R>(it, p, c);
         if (sb.lin >= 0) last = sb;
-        issue_from<LPR, GPL>(b, sb.lin >= 0 ? sb : last, p, lane);
+        issue_from<LPR, GPL, SBLK>(b, sb.lin >= 0 ? sb : last, lane);
         if (sa.lin < 0 && sb.lin < 0) break;
     }
 }
@@ -133,8 +156,10 @@ __device__ __forceinline__ void run_range(const DecodePlan& p, const DecodeClass
 
 // The plan arrays arrive as separate read-only, non-aliasing arguments, so
 // every table read is a scalar load with a wave-uniform value.
+// Three waves per SIMD fit the narrow variant without spilling; the wide
+// one (up to eight groups of x per lane) stays at two.
 template <int MAXG>
-__global__ __launch_bounds__(kBlock) void grouped_m1_kernel(const DecodeEntry* __restrict__ entries,
+__global__ __launch_bounds__(kBlock, MAXG <= 4 ? 3 : 2) void grouped_m1_kernel(const DecodeEntry* __restrict__ entries,
                                                             const DecodeClass* __restrict__ classes,
                                                             const int32_t* __restrict__ class_lin, int nclasses) {
     DecodePlan p;
@@ -155,8 +180,16 @@ __global__ __launch_bounds__(kBlock) void grouped_m1_kernel(const DecodeEntry* _
     const int64_t begin = i * c.steps / c.waves;
     const int64_t end = (i + 1) * c.steps / c.waves;
     if (begin >= end) return;
-#define WQ_RUN(L, G) \
-    if (c.lpr == L && c.gpl == G) { run_range<L, G, MAXG>(p, c, begin, end, lane); return; }
+    __shared__ __align__(16) uint16_t s_scales[kWavesPerBlock][kScaleBlockBytes / 2];
+    uint16_t* lds = s_scales[threadIdx.x / kWave];
+#define WQ_RUN(L, G)                                                    \
+    if (c.lpr == L && c.gpl == G) {                                     \
+        if (c.sblk)                                                     \
+            run_range<L, G, MAXG, true>(p, c, begin, end, lds, lane);   \
+        else                                                            \
+            run_range<L, G, MAXG, false>(p, c, begin, end, lds, lane);  \
+        return;                                                         \
+    }
     if constexpr (MAXG <= 4) {
         WQ_SHAPES_4(WQ_RUN)
     } else {
