@@ -190,14 +190,12 @@ GroupPlan plan_group(const std::vector<wq_linear>& lin, const Group& g, int capa
         e.lpr = lpr;
         e.gpl = gpl;
         max_gpl = std::max(max_gpl, gpl);
-        const int sblk = e.ng % 8 == 0 && (reinterpret_cast<uintptr_t>(l.scales) & 15) == 0;
         int ci = 0;
-        while (ci < (int)cls.size() && !(cls[ci].lpr == lpr && cls[ci].gpl == gpl && cls[ci].sblk == sblk)) ++ci;
+        while (ci < (int)cls.size() && !(cls[ci].lpr == lpr && cls[ci].gpl == gpl)) ++ci;
         if (ci == (int)cls.size()) {
             wq::DecodeClass c{};
             c.lpr = lpr;
-            c.gpl = (int16_t)gpl;
-            c.sblk = (int16_t)sblk;
+            c.gpl = gpl;
             cls.push_back(c);
             members.emplace_back();
             work.push_back(0.0);
@@ -216,6 +214,11 @@ GroupPlan plan_group(const std::vector<wq_linear>& lin, const Group& g, int capa
     for (size_t c = 0; c < cls.size(); ++c) {
         int64_t wc = (int64_t)(capacity * work[c] / total);
         wc = std::max<int64_t>(1, std::min<int64_t>(wc, cls[c].steps));
+        // A wave stages at most kYRows rows of y: at most that many rows' worth
+        // of steps per wave, even if the class then gets more waves than its
+        // share of the device.
+        const int64_t max_steps = wq::dev::kYRows / rows_per_step(cls[c].lpr, cls[c].gpl);
+        wc = std::max<int64_t>(wc, (cls[c].steps + max_steps - 1) / max_steps);
         cls[c].waves_begin = waves;
         cls[c].waves = (int32_t)wc;
         waves += (int)wc;

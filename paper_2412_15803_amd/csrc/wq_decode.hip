@@ -10,10 +10,11 @@
 // equal share of that class's steps (classes get waves in proportion to
 // their bytes).  A wave therefore streams one long contiguous range of rows,
 // crossing linear boundaries only where its range does, through a loop
-// specialised for its class's shape: two register buffers (compute A, refill
-// A, compute B, refill B), so the next step's weights -- of this linear or
-// the next one -- are always in flight while the current step is computed.
-// No atomics, no waiting between waves.
+// specialised for its class's shape: two or three register buffers (compute
+// a buffer, refill it with the step that many ahead, go on to the next), so
+// later steps' weights -- of this linear or the next one -- are always in
+// flight while the current step is computed.  Outputs are staged in LDS and
+// written per linear.  No atomics, no waiting between waves.
 #include "wq_device.h"
 #include "wq_internal.h"
 
@@ -84,44 +85,62 @@ __device__ __forceinline__ Step next_step(StepIter& it, const DecodePlan& p, con
     return s;
 }
 
-// The wave's x registers and the linear they belong to.  x is switched when
-// the wave computes the first step of another linear; every earlier step has
-// been computed by then, and the fresh x loads are the youngest in flight,
-// so the wave waits for its pipeline once per linear it enters.
+// The wave's x registers, the linear they belong to, and the rows of that
+// linear's y staged in LDS ([ybase, yend) of y).  x is switched when the wave
+// computes the first step of another linear: the staged rows of the previous
+// one are written out, and the fresh x loads are the youngest in flight, so
+// the wave waits for its pipeline once per linear it enters.
 template <int MAXG>
 struct XSlot {
     half2v xr[MAXG][16];
     int lin;
+    uint16_t* y;
+    int64_t ybase, yend;
 };
 
-template <int LPR, int GPL, int MAXG, bool SBLK>
-__device__ __forceinline__ void compute_from(const StepBuf& b, XSlot<MAXG>& xs, const Step& s, uint16_t* lds,
+template <int LPR, int GPL, int MAXG>
+__device__ __forceinline__ void compute_from(const StepBuf& b, XSlot<MAXG>& xs, const Step& s, uint16_t* ylds,
                                              int lane) {
     if (s.lin < 0) return;
     if (xs.lin != s.lin) {
+        if (xs.lin >= 0) flush_y(xs.y, xs.ybase, ylds, (int)(xs.yend - xs.ybase), lane);
         load_x_lane<LPR, GPL, MAXG>(s.x, s.ng, lane, xs.xr);
         xs.lin = s.lin;
+        xs.y = s.y;
+        xs.ybase = s.row;
     }
-    compute_step<LPR, GPL, MAXG, SBLK>(b, xs.xr, s.y, s.row, s.nrows, s.ng, lds, lane);
+    compute_step<LPR, GPL, MAXG>(b, xs.xr, s.nrows, ylds, (int)(s.row - xs.ybase), lane);
+    xs.yend = s.row + s.nrows;
 }
 
 // Issues are unconditional: past the end of the range the wave re-loads its
 // last valid step (never computed), so every path through the loop issues
 // the same loads and the compiler's wait counts stay exact.
-template <int LPR, int GPL, bool SBLK>
+template <int LPR, int GPL>
 __device__ __forceinline__ void issue_from(StepBuf& b, const Step& s, int lane) {
-    issue_step<LPR, GPL, SBLK>(b, s.packed, s.scales, s.row, s.row + s.nrows - 1, s.ng, lane);
+    issue_step<LPR, GPL>(b, s.packed, s.scales, s.row, s.row + s.nrows - 1, s.ng, lane);
 }
 
-template <int LPR, int GPL, int MAXG, bool SBLK>
+// Register buffers in the pipeline: three where a step holds at most six
+// groups per lane and the x registers are those of the narrow kernel
+// (the third buffer then still fits three waves per SIMD), else two.
+template <int LPR, int GPL, int MAXG>
+constexpr int pipeline_depth() {
+    return (MAXG <= 4 && StepShape<LPR, GPL>::U * GPL <= 6) ? 3 : 2;
+}
+
+// The plan keeps every wave's range at most kYRows / R steps, so the staged
+// rows of one linear always fit the wave's LDS slice.
+template <int LPR, int GPL, int MAXG>
 __device__ __forceinline__ void run_range(const DecodePlan& p, const DecodeClass& c, int64_t begin, int64_t end,
-                                          uint16_t* lds, int lane) {
+                                          uint16_t* ylds, int lane) {
     constexpr int R = StepShape<LPR, GPL>::ROWS;
+    constexpr int NB = pipeline_depth<LPR, GPL, MAXG>();
     StepIter it;
     it.pos = begin;
     it.end = end;
-    // Find the linear holding step `begin` (scalar binary search would do;
-    // the class lists are short, a forward scan is enough).
+    // Find the linear holding step `begin` (the class lists are short, a
+    // forward scan is enough).
     it.idx = 0;
     load_linear(it, p, c);
     while (begin >= it.lin_end) {
@@ -130,23 +149,28 @@ __device__ __forceinline__ void run_range(const DecodePlan& p, const DecodeClass
     }
     XSlot<MAXG> xs;
     xs.lin = -1;
-    StepBuf a, b;
-    Step sa = it.cur, sb = it.cur;
-    sa.lin = sb.lin = -1;
+    xs.y = nullptr;
+    xs.ybase = xs.yend = 0;
+    StepBuf buf[NB];
+    Step st[NB];
+#pragma unroll
+    for (int i = 0; i < NB; ++i) st[i].lin = -1;
     // The first pass only issues; afterwards each pass computes the step a
     // buffer holds and refills that buffer with the wave's next step.
     Step last = it.cur;  // the latest valid step (the range is never empty)
     for (;;) {
-        compute_from<LPR, GPL, MAXG, SBLK>(a, xs, sa, lds, lane);
-        sa = next_step<R>(it, p, c);
-        if (sa.lin >= 0) last = sa;
-        issue_from<LPR, GPL, SBLK>(a, sa.lin >= 0 ? sa : last, lane);
-        compute_from<LPR, GPL, MAXG, SBLK>(b, xs, sb, lds, lane);
-        sb = next_step<R>(it, p, c);
-        if (sb.lin >= 0) last = sb;
-        issue_from<LPR, GPL, SBLK>(b, sb.lin >= 0 ? sb : last, lane);
-        if (sa.lin < 0 && sb.lin < 0) break;
+        bool any = false;
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+            compute_from<LPR, GPL, MAXG>(buf[i], xs, st[i], ylds, lane);
+            st[i] = next_step<R>(it, p, c);
+            if (st[i].lin >= 0) last = st[i];
+            any = any || st[i].lin >= 0;
+            issue_from<LPR, GPL>(buf[i], st[i].lin >= 0 ? st[i] : last, lane);
+        }
+        if (!any) break;
     }
+    if (xs.lin >= 0) flush_y(xs.y, xs.ybase, ylds, (int)(xs.yend - xs.ybase), lane);
 }
 
 // The (lanes per row, groups per lane) shapes a launch supports: those with
@@ -180,16 +204,10 @@ __global__ __launch_bounds__(kBlock, MAXG <= 4 ? 3 : 2) void grouped_m1_kernel(c
     const int64_t begin = i * c.steps / c.waves;
     const int64_t end = (i + 1) * c.steps / c.waves;
     if (begin >= end) return;
-    __shared__ __align__(16) uint16_t s_scales[kWavesPerBlock][kScaleBlockBytes / 2];
-    uint16_t* lds = s_scales[threadIdx.x / kWave];
-#define WQ_RUN(L, G)                                                    \
-    if (c.lpr == L && c.gpl == G) {                                     \
-        if (c.sblk)                                                     \
-            run_range<L, G, MAXG, true>(p, c, begin, end, lds, lane);   \
-        else                                                            \
-            run_range<L, G, MAXG, false>(p, c, begin, end, lds, lane);  \
-        return;                                                         \
-    }
+    __shared__ __align__(16) uint16_t s_y[kWavesPerBlock][kYRows];
+    uint16_t* ylds = s_y[threadIdx.x / kWave];
+#define WQ_RUN(L, G) \
+    if (c.lpr == L && c.gpl == G) { run_range<L, G, MAXG>(p, c, begin, end, ylds, lane); return; }
     if constexpr (MAXG <= 4) {
         WQ_SHAPES_4(WQ_RUN)
     } else {

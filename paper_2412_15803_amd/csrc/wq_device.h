@@ -129,14 +129,11 @@ struct StepShape {
     static constexpr int ROWS = U * SLOTS;            // rows per step
 };
 
-// One step's loads.  Scales arrive either per lane (s[], one 2-byte load per
-// group and row) or, when the step's scales form 16-byte-aligned whole
-// chunks, as this lane's 16 bytes of the step's contiguous scale block
-// (sblk), handed to the lanes through LDS at compute time.
+// One step's loads: per row and group, the 16-byte group of codes and its
+// 2-byte scale.
 struct StepBuf {
     u32x4 w[8];
     uint32_t s[8];
-    u32x4 sblk;
 };
 
 // Orders one wave's LDS accesses across its lanes: a wave's LDS operations
@@ -147,10 +144,6 @@ __device__ __forceinline__ void wave_lds_sync() {
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
-
-// Bytes of LDS per wave for the scale block of one step: at most
-// rows-per-step * groups-per-row = U * 64 * GPL <= 512 scales.
-constexpr int kScaleBlockBytes = 1024;
 
 // x groups of this lane: every group's loads are issued before any is
 // rearranged, so they share one round trip.  Lanes whose group index runs
@@ -180,12 +173,8 @@ __device__ __forceinline__ void load_x_lane(const uint16_t* x, int ng, int lane,
 }
 
 // Issue the loads of rows [row0, row0 + ROWS) (clamped to last_row, so every
-// lane always loads a valid address and no branch is needed).  With SBLK the
-// scales of the step are one contiguous block of ROWS * ng halves starting
-// at row0 * ng, loaded as 16-byte chunks (ng % 8 == 0 and a 16-byte aligned
-// scale array make every chunk whole), one per lane; chunk indices are
-// clamped to the last chunk of last_row.
-template <int LPR, int GPL, bool SBLK>
+// lane always loads a valid address and no branch is needed).
+template <int LPR, int GPL>
 __device__ __forceinline__ void issue_step(StepBuf& b, const u32x4* packed, const uint16_t* scales,
                                            int64_t row0, int64_t last_row, int ng, int lane) {
     using S = StepShape<LPR, GPL>;
@@ -201,12 +190,8 @@ __device__ __forceinline__ void issue_step(StepBuf& b, const u32x4* packed, cons
             const int g = min(sub + LPR * j, ng - 1);
             const int64_t idx = r * ng + g;
             b.w[u * GPL + j] = gp[idx];
-            if constexpr (!SBLK) b.s[u * GPL + j] = gs[idx];
+            b.s[u * GPL + j] = gs[idx];
         }
-    }
-    if constexpr (SBLK) {
-        const int64_t chunk = min(row0 * (ng / 8) + lane, (last_row + 1) * (ng / 8) - 1);
-        b.sblk = gbl(reinterpret_cast<const u32x4*>(scales))[chunk];
     }
     // Keep this step's loads ahead of anything issued later: the load counter
     // retires in issue order, so a later step's loads must not be scheduled
@@ -217,44 +202,44 @@ __device__ __forceinline__ void issue_step(StepBuf& b, const u32x4* packed, cons
     __builtin_amdgcn_sched_barrier(0);
 }
 
-// Dot products, segment reduction and fp16 store of one step; only rows
-// below row0 + nrows are written.  Lanes past the row's groups hold zero x,
-// so their (clamped, finite) codes contribute nothing.  With SBLK the step's
-// scale block goes through `lds` (this wave's kScaleBlockBytes): each lane
-// stores its chunk, then reads the scales of its own rows and groups.
-template <int LPR, int GPL, int MAXG, bool SBLK>
-__device__ __forceinline__ void compute_step(const StepBuf& b, const half2v (&xr)[MAXG][16], uint16_t* __restrict__ y,
-                                             int64_t row0, int nrows, int ng, uint16_t* lds, int lane) {
+// Dot products, segment reduction and fp16 rounding of one step; the rows
+// below nrows are staged in this wave's LDS slice at ylds[yrel + row], to be
+// written out by flush_y.  (Global stores inside the loop would share the
+// load counter with the weight loads in flight, and every later wait for a
+// step's loads would then also wait for those stores.)  Lanes past the
+// row's groups hold zero x, so their (clamped, finite) codes contribute
+// nothing.
+template <int LPR, int GPL, int MAXG>
+__device__ __forceinline__ void compute_step(const StepBuf& b, const half2v (&xr)[MAXG][16], int nrows,
+                                             uint16_t* ylds, int yrel, int lane) {
     using S = StepShape<LPR, GPL>;
     const int slot = lane / LPR;
     const int sub = lane & (LPR - 1);
-    uint16_t sv[S::U * GPL];
-    if constexpr (SBLK) {
-        // The block's 16-byte chunk c covers scales [8c, 8c + 8) of the step.
-        if (lane * 8 < S::ROWS * ng) *reinterpret_cast<u32x4*>(lds + lane * 8) = b.sblk;
-        wave_lds_sync();
-#pragma unroll
-        for (int u = 0; u < S::U; ++u)
-#pragma unroll
-            for (int j = 0; j < GPL; ++j)
-                sv[u * GPL + j] = lds[(slot * S::U + u) * ng + min(sub + LPR * j, ng - 1)];
-    } else {
-#pragma unroll
-        for (int i = 0; i < S::U * GPL; ++i) sv[i] = (uint16_t)b.s[i];
-    }
 #pragma unroll
     for (int u = 0; u < S::U; ++u) {
         float acc = 0.0f;
 #pragma unroll
         for (int j = 0; j < GPL; ++j) {
-            const float s = __half2float(__ushort_as_half(sv[u * GPL + j]));
+            const float s = __half2float(__ushort_as_half((uint16_t)b.s[u * GPL + j]));
             acc = fmaf(s, dot_group(b.w[u * GPL + j], xr[j]), acc);
         }
         const float tot = segment_sum<LPR>(acc);
         const int rr = slot * S::U + u;
-        if ((lane & (LPR - 1)) == LPR - 1 && rr < nrows) gbl(y)[row0 + rr] = __half_as_ushort(__float2half_rn(tot));
+        if (sub == LPR - 1 && rr < nrows) ylds[yrel + rr] = __half_as_ushort(__float2half_rn(tot));
     }
-    if constexpr (SBLK) wave_lds_sync();  // reads before the next step's stores
+}
+
+// Rows of y a wave stages in LDS before writing them out (2 KiB per wave).
+// Every rows-per-step value divides it.
+constexpr int kYRows = 1024;
+
+// Write the `count` staged rows ylds[0, count) to y[row0, row0 + count),
+// 64 consecutive rows per store instruction.
+__device__ __forceinline__ void flush_y(uint16_t* y, int64_t row0, const uint16_t* ylds, int count, int lane) {
+    wave_lds_sync();
+    WQ_GLOBAL uint16_t* dst = gbl(y) + row0;
+    for (int i = lane; i < count; i += kWave) dst[i] = ylds[i];
+    wave_lds_sync();  // stores have read the slice before it is refilled
 }
 
 // Lanes per row and groups per lane for a row of ng groups (ng <= 512):

@@ -37,9 +37,7 @@ static_assert(sizeof(DecodeEntry) == 72, "DecodeEntry layout");
 // split into `waves` equal contiguous ranges, one per wave, for the waves
 // [waves_begin, waves_begin + waves) of the grid.
 struct DecodeClass {
-    int32_t lpr;          // the class's step shape: lanes per row,
-    int16_t gpl;          //   groups per lane,
-    int16_t sblk;         //   scales loaded per step as one block (ng % 8 == 0, aligned)
+    int32_t lpr, gpl;     // the class's step shape
     int32_t first;        // offset of its linears in the class list
     int32_t count;        // number of linears
     int64_t steps;        // steps over all its linears

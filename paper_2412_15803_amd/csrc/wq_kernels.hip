@@ -61,15 +61,12 @@ __global__ __launch_bounds__(kBlock) void pack_kernel(const float* __restrict__ 
 
 // ------------------------------------------------------------ batch-1 GEMV
 //
-// Each wave owns a contiguous block of rows and walks it in steps through two
-// register buffers: compute buffer A, refill A with the step two ahead,
-// compute B, refill B.  Whenever the wave waits for a buffer, the other
-// buffer's loads are still in flight.
-//
-// SBLK: the scales of a step are loaded as one contiguous block (one 16-byte
-// load per lane) and spread to the lanes through LDS; needs ng % 8 == 0 and a
-// 16-byte aligned scale array.
-template <int LPR, int GPL, bool SBLK>
+// Each wave owns a contiguous block of at most kYRows rows and walks it in
+// steps through two register buffers: compute buffer A, refill A with the
+// step two ahead, compute B, refill B.  Whenever the wave waits for a buffer,
+// the other buffer's loads are still in flight.  Outputs are staged in LDS
+// and written once, after the last step.
+template <int LPR, int GPL>
 __global__ __launch_bounds__(kBlock) void gemv_m1_kernel(const u32x4* packed, const uint16_t* scales,
                                                          const uint16_t* __restrict__ x,
                                                          uint16_t* __restrict__ y, int64_t n, int ng,
@@ -85,8 +82,8 @@ __global__ __launch_bounds__(kBlock) void gemv_m1_kernel(const u32x4* packed, co
     const int64_t last = re - 1;
     const int64_t steps = (re - rb + R - 1) / R;
 
-    __shared__ __align__(16) uint16_t s_scales[kWavesPerBlock][kScaleBlockBytes / 2];
-    uint16_t* lds = s_scales[threadIdx.x / kWave];
+    __shared__ __align__(16) uint16_t s_y[kWavesPerBlock][kYRows];
+    uint16_t* ylds = s_y[threadIdx.x / kWave];
 
     half2v xr[GPL][16];
     load_x_lane<LPR, GPL, GPL>(x, ng, lane, xr);
@@ -99,13 +96,14 @@ __global__ __launch_bounds__(kBlock) void gemv_m1_kernel(const u32x4* packed, co
     StepBuf a, b;
     for (int64_t s = -2; s < steps; s += 2) {
         const int64_t ra = rb + s * R;
-        if (s >= 0) compute_step<LPR, GPL, GPL, SBLK>(a, xr, y, ra, (int)min((int64_t)R, re - ra), ng, lds, lane);
-        issue_step<LPR, GPL, SBLK>(a, packed, scales, ra + 2 * R, last, ng, lane);
+        if (s >= 0) compute_step<LPR, GPL, GPL>(a, xr, (int)min((int64_t)R, re - ra), ylds, (int)(s * R), lane);
+        issue_step<LPR, GPL>(a, packed, scales, ra + 2 * R, last, ng, lane);
         const int64_t rbb = ra + R;
         if (s + 1 >= 0 && s + 1 < steps)
-            compute_step<LPR, GPL, GPL, SBLK>(b, xr, y, rbb, (int)min((int64_t)R, re - rbb), ng, lds, lane);
-        issue_step<LPR, GPL, SBLK>(b, packed, scales, rbb + 2 * R, last, ng, lane);
+            compute_step<LPR, GPL, GPL>(b, xr, (int)min((int64_t)R, re - rbb), ylds, (int)((s + 1) * R), lane);
+        issue_step<LPR, GPL>(b, packed, scales, rbb + 2 * R, last, ng, lane);
     }
+    flush_y(y, rb, ylds, (int)(re - rb), lane);
 }
 
 // ------------------------------------------------------- generic GEMV (any M)
@@ -158,16 +156,14 @@ hipError_t launch_m1(const uint32_t* packed, const uint16_t* scales, const uint1
                      int64_t n, int64_t ng, hipStream_t stream) {
     constexpr int R = StepShape<LPR, GPL>::ROWS;
     const int64_t steps = (n + R - 1) / R;
-    const int64_t steps_per_wave = (steps + kTargetWaves - 1) / kTargetWaves;
+    // At most kYRows rows per wave (its LDS staging of y); more waves than
+    // the target when the matrix is taller than that allows.
+    const int64_t steps_per_wave = min((steps + kTargetWaves - 1) / kTargetWaves, (int64_t)(kYRows / R));
     const int64_t rows_per_wave = steps_per_wave * R;
     const int64_t waves = (n + rows_per_wave - 1) / rows_per_wave;
     const int64_t blocks = (waves + kWavesPerBlock - 1) / kWavesPerBlock;
-    if (ng % 8 == 0 && (reinterpret_cast<uintptr_t>(scales) & 15) == 0)
-        hipLaunchKernelGGL((gemv_m1_kernel<LPR, GPL, true>), dim3((unsigned)blocks), dim3(kBlock), 0, stream,
-                           reinterpret_cast<const u32x4*>(packed), scales, x, y, n, (int)ng, rows_per_wave);
-    else
-        hipLaunchKernelGGL((gemv_m1_kernel<LPR, GPL, false>), dim3((unsigned)blocks), dim3(kBlock), 0, stream,
-                           reinterpret_cast<const u32x4*>(packed), scales, x, y, n, (int)ng, rows_per_wave);
+    hipLaunchKernelGGL((gemv_m1_kernel<LPR, GPL>), dim3((unsigned)blocks), dim3(kBlock), 0, stream,
+                       reinterpret_cast<const u32x4*>(packed), scales, x, y, n, (int)ng, rows_per_wave);
     return hipGetLastError();
 }
 
