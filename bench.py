@@ -22,6 +22,10 @@ import sys
 import time
 
 HBM_PEAK_GBS = 8000.0
+ROOT = os.path.dirname(os.path.abspath(__file__))
+# rocprofv3 summary of the step kernel (duration, FETCH_SIZE / WRITE_SIZE);
+# its traffic figure is used only while the library sources still match.
+STEP_PROFILE = os.path.join(ROOT, "profiles", "grouped_m1_3b_step.md")
 METRIC = "achieved HBM GB/s (% of peak) & µs per decode step of 4-bit linears, batch 1"
 
 
@@ -138,6 +142,18 @@ def cpu_baseline(seed, budget_s):
     }
 
 
+def profiled_traffic():
+    """HBM bytes per step launch from the committed counter summary, or None
+    when the kernels changed since the counters were taken."""
+    from paper_2412_15803_amd.build import source_hash
+    from paper_2412_15803_amd.profsum import parse_traffic
+
+    got = parse_traffic(STEP_PROFILE)
+    if got is None or got[0] != source_hash():
+        return None
+    return got[1]
+
+
 def copy_probe(mib, device):
     import torch
 
@@ -192,7 +208,7 @@ def main():
         "peak": HBM_PEAK_GBS,
         "unit": "GB/s",
         "frac": round(gbs / HBM_PEAK_GBS, 4),
-        "traffic": None,
+        "traffic": profiled_traffic(),
         "kernel": f"grouped_m1_kernel (one launch per step, avg {ms_per_step * 1e3:.2f} us, "
                   f"{step_bytes / 1e6:.2f} MB algorithmic per launch)",
     }

@@ -1,0 +1,135 @@
+"""Summarise rocprofv3 output for one kernel into a short markdown file.
+
+    python -m paper_2412_15803_amd.profsum --kernel grouped_m1_kernel \
+        --trace <dir with *_kernel_trace.csv> --fetch <dir of a --pmc FETCH_SIZE run> \
+        --write <dir of a --pmc WRITE_SIZE run> --algo-bytes N --copy-mib C \
+        --command "<the rocprofv3 command>" --out profiles/<name>.md
+
+Durations come from the kernel trace.  HBM traffic per launch is FETCH_SIZE
+and WRITE_SIZE (KiB per dispatch) scaled by what the same counters read for a
+plain device copy of C MiB in the same run (its true traffic is C MiB read and
+C MiB written).  The summary records the library's source hash; bench.py
+reports the traffic figure only while the sources still match it.
+"""
+
+from __future__ import annotations
+
+import argparse
+import csv
+import glob
+import os
+import statistics
+
+from .build import source_hash
+
+
+def _rows(directory, pattern):
+    out = []
+    for f in sorted(glob.glob(os.path.join(directory, "**", pattern), recursive=True)):
+        with open(f, newline="") as fh:
+            out.extend(csv.DictReader(fh))
+    return out
+
+
+def _counter(directory, name):
+    """[(kernel name, grid size, value)] for one counter, one entry per dispatch."""
+    return [(r["Kernel_Name"], int(r["Grid_Size"]), float(r["Counter_Value"]))
+            for r in _rows(directory, "*counter_collection.csv") if r["Counter_Name"] == name]
+
+
+def _copy_value(entries):
+    copies = [v for name, _, v in entries if "copy" in name.lower()]
+    if not copies:
+        raise SystemExit("no copy kernel found in the counter run (bench.py --copy-probe-mib)")
+    return max(copies)
+
+
+def summarise(args):
+    trace = [r for r in _rows(args.trace, "*kernel_trace.csv") if args.kernel in r["Kernel_Name"]]
+    if not trace:
+        raise SystemExit(f"kernel {args.kernel!r} not in the trace")
+    durs = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in trace]
+    fetch = _counter(args.fetch, "FETCH_SIZE")
+    write = _counter(args.write, "WRITE_SIZE")
+    copy_kib = args.copy_mib * 1024.0
+    f_scale = copy_kib / _copy_value(fetch)
+    w_scale = copy_kib / _copy_value(write)
+    kf = [v for name, _, v in fetch if args.kernel in name]
+    kw = [v for name, _, v in write if args.kernel in name]
+    if not kf or not kw:
+        raise SystemExit(f"kernel {args.kernel!r} not in the counter runs")
+    fetch_b = statistics.mean(kf) * f_scale * 1024.0
+    write_b = statistics.mean(kw) * w_scale * 1024.0
+    traffic = fetch_b + write_b
+    avg = statistics.mean(durs)
+    lines = [
+        f"# {args.title}",
+        "",
+        "Commands (each from /tmp with TMPDIR=/tmp, one MI355X):",
+        "",
+        "```",
+        *args.command,
+        "```",
+        "",
+        "| Figure | Value |",
+        "|---|---|",
+        f"| kernel | `{args.kernel}` |",
+        f"| launches in the trace | {len(durs)} |",
+        f"| duration avg / min / max (us) | {avg:.2f} / {min(durs):.2f} / {max(durs):.2f} |",
+        f"| algorithmic bytes per launch | {args.algo_bytes:,} |",
+        f"| achieved (algorithmic bytes / avg duration) | {args.algo_bytes / (avg * 1e3):.1f} GB/s |",
+        f"| FETCH_SIZE per launch (raw KiB, mean of {len(kf)}) | {statistics.mean(kf):,.1f} |",
+        f"| WRITE_SIZE per launch (raw KiB, mean of {len(kw)}) | {statistics.mean(kw):,.1f} |",
+        f"| copy calibration: FETCH_SIZE / WRITE_SIZE of a {args.copy_mib} MiB copy (raw KiB) | "
+        f"{_copy_value(fetch):,.1f} / {_copy_value(write):,.1f} |",
+        f"| scale factors applied (fetch / write) | {f_scale:.4f} / {w_scale:.4f} |",
+        f"| HBM traffic per launch, scaled (fetch + write bytes) | {fetch_b:,.0f} + {write_b:,.0f} = {traffic:,.0f} |",
+        f"| traffic / algorithmic bytes | {traffic / args.algo_bytes:.4f} |",
+        "",
+        "Machine-readable (read by bench.py; valid only for this source hash):",
+        "",
+        "```",
+        f"source_hash: {source_hash()}",
+        f"traffic_bytes_per_launch: {traffic:.0f}",
+        f"avg_duration_us: {avg:.3f}",
+        "```",
+        "",
+    ]
+    with open(args.out, "w") as fh:
+        fh.write("\n".join(lines))
+    print("\n".join(lines))
+
+
+def parse_traffic(path):
+    """(source_hash, traffic bytes per launch) from a summary written above, or None."""
+    try:
+        with open(path) as fh:
+            text = fh.read()
+    except OSError:
+        return None
+    vals = {}
+    for line in text.splitlines():
+        if ":" in line:
+            k, _, v = line.partition(":")
+            vals[k.strip()] = v.strip()
+    if "source_hash" not in vals or "traffic_bytes_per_launch" not in vals:
+        return None
+    return vals["source_hash"], float(vals["traffic_bytes_per_launch"])
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--kernel", required=True, help="substring of the kernel name")
+    ap.add_argument("--trace", required=True)
+    ap.add_argument("--fetch", required=True)
+    ap.add_argument("--write", required=True)
+    ap.add_argument("--algo-bytes", type=int, required=True)
+    ap.add_argument("--copy-mib", type=int, required=True)
+    ap.add_argument("--command", action="append", required=True)
+    ap.add_argument("--title", default="Kernel trace and HBM traffic")
+    ap.add_argument("--out", required=True)
+    summarise(ap.parse_args())
+
+
+if __name__ == "__main__":
+    main()
