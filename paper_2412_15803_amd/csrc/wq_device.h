@@ -68,19 +68,26 @@ __device__ __forceinline__ uint32_t and_or(uint32_t w, uint32_t mask, uint32_t m
     return r;
 }
 
-__device__ __forceinline__ float dot_word(uint32_t w, const half2v* xp, float acc) {
+// The eight codes of one word as exact fp16 (q - 8) pairs, ordered
+// (0, 4), (1, 5), (2, 6), (3, 7).
+__device__ __forceinline__ void dequant_word(uint32_t w, half2v (&q)[4]) {
     const half2v k1032 = {(_Float16)1032.0f, (_Float16)1032.0f};
     const half2v k1_16 = {(_Float16)0.0625f, (_Float16)0.0625f};
     const half2v km72 = {(_Float16)-72.0f, (_Float16)-72.0f};
     const uint32_t w8 = w >> 8;
-    const half2v q04 = as_h2(and_or(w, 0x000F000Fu, 0x64006400u)) - k1032;
-    const half2v q15 = as_h2(and_or(w, 0x00F000F0u, 0x64006400u)) * k1_16 + km72;
-    const half2v q26 = as_h2(and_or(w8, 0x000F000Fu, 0x64006400u)) - k1032;
-    const half2v q37 = as_h2(and_or(w8, 0x00F000F0u, 0x64006400u)) * k1_16 + km72;
-    acc = __builtin_amdgcn_fdot2(q04, xp[0], acc, false);
-    acc = __builtin_amdgcn_fdot2(q15, xp[1], acc, false);
-    acc = __builtin_amdgcn_fdot2(q26, xp[2], acc, false);
-    acc = __builtin_amdgcn_fdot2(q37, xp[3], acc, false);
+    q[0] = as_h2(and_or(w, 0x000F000Fu, 0x64006400u)) - k1032;
+    q[1] = as_h2(and_or(w, 0x00F000F0u, 0x64006400u)) * k1_16 + km72;
+    q[2] = as_h2(and_or(w8, 0x000F000Fu, 0x64006400u)) - k1032;
+    q[3] = as_h2(and_or(w8, 0x00F000F0u, 0x64006400u)) * k1_16 + km72;
+}
+
+__device__ __forceinline__ float dot_word(uint32_t w, const half2v* xp, float acc) {
+    half2v q[4];
+    dequant_word(w, q);
+    acc = __builtin_amdgcn_fdot2(q[0], xp[0], acc, false);
+    acc = __builtin_amdgcn_fdot2(q[1], xp[1], acc, false);
+    acc = __builtin_amdgcn_fdot2(q[2], xp[2], acc, false);
+    acc = __builtin_amdgcn_fdot2(q[3], xp[3], acc, false);
     return acc;
 }
 

@@ -16,6 +16,10 @@ hipError_t launch_gemv(const uint32_t* packed, const uint16_t* scales,
                        const uint16_t* x, uint16_t* y,
                        int64_t n, int64_t k, int64_t m, hipStream_t stream);
 
+// y[M][N] for 2 <= M on the matrix cores, 16 batch rows per launch.
+hipError_t launch_gemm_mfma(const uint32_t* packed, const uint16_t* scales, const uint16_t* x, uint16_t* y,
+                            int64_t n, int64_t k, int64_t m, hipStream_t stream);
+
 // One linear of a grouped launch as the kernel sees it (built on the host,
 // uploaded once per distinct descriptor list).
 struct DecodeEntry {
