@@ -95,9 +95,13 @@ wq_status wq_pack(const float* w, uint32_t* packed_w, uint16_t* scales,
  *   y         [M][N] fp16 bits, device, 2-byte aligned, written.
  *   N, K, M   1 <= N <= WQ_MAX_N, 32 <= K <= WQ_MAX_K, 1 <= M <= WQ_MAX_M.
  *   group     must be 32.
- * Accumulation is fp32 with exact products; each output is rounded once to
- * fp16 (round to nearest even).  Per element the result is within
- * 1e-3 * sum_k |w_hat[n][k] x[m][k]| + 1e-5 of the exactly rounded value.
+ * Accumulation is fp32; each output is rounded once to fp16 (round to
+ * nearest even).  For M == 1 every product is exact.  For M >= 2 (matrix
+ * cores) each scaled weight (q - 8) * s is first rounded to fp16 (relative
+ * error <= 2^-11); this needs |(q - 8) * s| <= 65504, i.e. scales below 8188,
+ * and larger scales give infinities on that path.  Per element the result is
+ * within 1e-3 * sum_k |w_hat[n][k] x[m][k]| + 1e-5 of the exactly rounded
+ * value.
  * y must not overlap x, packed_w or scales.
  * Errors: INVALID_ARG, UNSUPPORTED, MISALIGNED, HIP (as for wq_pack).
  */
