@@ -42,6 +42,8 @@ def parse_args():
                     help="also time the step with every linear reading its predecessor's output")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (for scaling HBM counters)")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the per-shape figures (single linears, small batches, 8B-class step)")
     return ap.parse_args()
 
 
@@ -142,6 +144,109 @@ def cpu_baseline(seed, budget_s):
     }
 
 
+def random_linear(n, k, gen, device):
+    """Random packed codes and scales of one linear (timing inputs: the GEMV's
+    cost does not depend on the values)."""
+    import torch
+
+    p = torch.randint(-2**31, 2**31 - 1, (n, k // 8), dtype=torch.int32, device=device, generator=gen)
+    s = (torch.rand((n, k // 32), device=device, generator=gen) * 0.01 + 0.001).to(torch.float16)
+    return p, s
+
+
+def time_gemv_rotated(n, k, ms_list, gen, device, calls=200, reps=5):
+    """Per-call time of wq_gemv on one shape, cold: the calls rotate over
+    copies of the weights totalling >= 1 GiB (4x the 256 MB last-level cache)
+    and are replayed from a HIP graph, so host launch cost is not counted.
+    Returns {M: (us per call, GB/s)} for each M in ms_list."""
+    import torch
+
+    from paper_2412_15803_amd import workloads as wl
+    from paper_2412_15803_amd import wq
+
+    per = wl.ideal_bytes(n, k, 1)
+    r = max(1, -(-(1 << 30) // per))
+    ws = [random_linear(n, k, gen, device) for _ in range(r)]
+    out = {}
+    for m in ms_list:
+        x = torch.randn((m, k), device=device, generator=gen).to(torch.float16)
+        y = torch.empty((m, n), dtype=torch.float16, device=device)
+        side = torch.cuda.Stream(device)
+        side.wait_stream(torch.cuda.current_stream(device))
+        with torch.cuda.stream(side):
+            for i in range(3):
+                wq.wq_gemv(*ws[i % r], x, y)
+        torch.cuda.current_stream(device).wait_stream(side)
+        torch.cuda.synchronize()
+        eager = y.clone()
+        wq.wq_gemv(*ws[(calls - 1) % r], x, eager)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for i in range(calls):
+                wq.wq_gemv(*ws[i % r], x, y)
+        times = []
+        for _ in range(reps):
+            a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            graph.replay()
+            e.record()
+            torch.cuda.synchronize()
+            times.append(a.elapsed_time(e) / calls)
+            if not torch.equal(y, eager):
+                raise RuntimeError(f"graph replay of wq_gemv {n}x{k} M={m} differs from the eager call")
+        ms = sorted(times)[len(times) // 2]
+        out[m] = (round(ms * 1e3, 2), round(wl.ideal_bytes(n, k, m) / (ms * 1e-3) / 1e9, 1))
+        del graph
+    del ws
+    torch.cuda.empty_cache()
+    return out
+
+
+def step_8b(gen, device, steps, warmup):
+    """The 8B-class decode step: 32 x (qkv 6144x4096, o 4096x4096, gate_up
+    28672x4096, down 4096x14336) + lm_head 128256x4096, random codes, M=1."""
+    import torch
+
+    from paper_2412_15803_amd import workloads as wl
+    from paper_2412_15803_amd import wq
+
+    shapes = [(lin.n, lin.k) for lin in wl.LLAMA8B_LAYER] * 32 + [(128256, 4096)]
+    lins, total = [], 0
+    for n, k in shapes:
+        p, s = random_linear(n, k, gen, device)
+        x = torch.randn((1, k), device=device, generator=gen).to(torch.float16)
+        lins.append((p, s, x, torch.empty((1, n), dtype=torch.float16, device=device)))
+        total += wl.ideal_bytes(n, k, 1)
+    ms = time_steps(lins, wq.make_linear_array(lins, 1), steps, warmup)
+    del lins
+    torch.cuda.empty_cache()
+    return {"linears": len(shapes), "bytes": total, "us": round(ms * 1e3, 2),
+            "GB_s": round(total / (ms * 1e-3) / 1e9, 1), "frac": round(total / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+
+
+def per_config(device, seed):
+    """Per-shape figures beside the headline step (SURVEY configs 1-4 and the
+    8B-class step); none of them is the bench value."""
+    import torch
+
+    from paper_2412_15803_amd import workloads as wl
+
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed + 7)
+    res = {"method": "single wq_gemv calls rotated over >= 1 GiB of weight copies, replayed from a HIP graph "
+                     "(device time per call, host launch excluded); random codes and scales of each shape"}
+    res["512x512 M=1"] = time_gemv_rotated(512, 512, [1], gen, device)[1]
+    for lin in wl.LLAMA3B_LAYER + (wl.LLAMA3B_LM_HEAD,):
+        res[f"3B {lin.name} {lin.n}x{lin.k} M=1"] = time_gemv_rotated(lin.n, lin.k, [1], gen, device)[1]
+    for lin in wl.LLAMA8B_LAYER:
+        got = time_gemv_rotated(lin.n, lin.k, [1, 4, 8, 16], gen, device)
+        for m, v in got.items():
+            res[f"8B {lin.name} {lin.n}x{lin.k} M={m}"] = v
+    res["unit"] = "[us per call, GB/s]"
+    res["8B step M=1 (one wq_decode_linears call, 129 linears)"] = step_8b(gen, device, 50, 5)
+    return res
+
+
 def profiled_traffic():
     """HBM bytes per step launch from the committed counter summary, or None
     when the kernels changed since the counters were taken."""
@@ -213,6 +318,11 @@ def main():
                   f"{step_bytes / 1e6:.2f} MB algorithmic per launch)",
     }
 
+    configs = None
+    if not args.no_configs:
+        log("timing the per-shape figures (single linears, small batches, 8B-class step)")
+        configs = per_config(device, args.seed)
+
     cpu = None
     if not args.no_cpu_baseline:
         log(f"timing the CPU oracle (~{args.cpu_seconds:.0f} s sample)")
@@ -244,6 +354,7 @@ def main():
         },
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "per_config": configs,
     }
     print(json.dumps(out), flush=True)
 

@@ -42,14 +42,13 @@ COMPILE_FLAGS = [
 
 
 def source_hash() -> str:
-    """Short hash of the HIP sources and headers the library is built from;
+    """Short hash of the HIP sources the kernels are built from (csrc/);
     profile summaries record it so that figures taken from an older kernel
     are recognised as stale."""
     import hashlib
 
     h = hashlib.sha256()
-    files = sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.h"))
-                   + glob.glob(os.path.join(INCLUDE, "*.h")))
+    files = sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.h")))
     for f in files:
         h.update(os.path.basename(f).encode())
         with open(f, "rb") as fh:
