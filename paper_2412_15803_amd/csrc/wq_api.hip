@@ -153,7 +153,7 @@ std::vector<Group> split_groups(const std::vector<wq_linear>& lin) {
     return groups;
 }
 
-int rows_per_step(int lpr, int gpl) { return (gpl >= 8 ? 1 : 8 / gpl) * (64 / lpr); }
+int rows_per_step(int lpr, int gpl) { return wq::dev::step_rows_per_slot(gpl) * (64 / lpr); }
 
 size_t align16(size_t v) { return (v + 15) & ~size_t(15); }
 

@@ -121,12 +121,21 @@ __device__ __forceinline__ void issue_from(StepBuf& b, const Step& s, int lane) 
     issue_step<LPR, GPL>(b, s.packed, s.scales, s.row, s.row + s.nrows - 1, s.ng, lane);
 }
 
-// Register buffers in the pipeline: three where a step holds at most six
-// groups per lane and the x registers are those of the narrow kernel
-// (the third buffer then still fits three waves per SIMD), else two.
+// Register buffers in the pipeline: as many steps as fit a budget of
+// in-flight 16-byte loads per lane (18 beside the narrow kernel's x
+// registers, which keeps three waves per SIMD; 14 beside the wide one's),
+// at least two and at most four.
+#ifndef WQ_DEPTH_BUDGET4
+#define WQ_DEPTH_BUDGET4 18
+#endif
+#ifndef WQ_DEPTH_BUDGET8
+#define WQ_DEPTH_BUDGET8 14
+#endif
 template <int LPR, int GPL, int MAXG>
 constexpr int pipeline_depth() {
-    return (MAXG <= 4 && StepShape<LPR, GPL>::U * GPL <= 6) ? 3 : 2;
+    constexpr int per_step = StepShape<LPR, GPL>::U * GPL;
+    constexpr int nb = (MAXG <= 4 ? WQ_DEPTH_BUDGET4 : WQ_DEPTH_BUDGET8) / per_step;
+    return nb < 2 ? 2 : (nb > 4 ? 4 : nb);
 }
 
 // The plan keeps every wave's range at most kYRows / R steps, so the staged

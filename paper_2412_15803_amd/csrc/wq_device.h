@@ -127,20 +127,31 @@ __device__ __forceinline__ float segment_sum(float v) {
 // 16 contiguous bytes of each slot's row.  LPR is chosen per shape so that
 // LPR * GPL covers the row's groups with no idle lanes where possible.
 //
-// A "step" is U rows per slot (U * 64/LPR rows per wave) and U * GPL <= 8
-// loads per lane; slot s takes rows row0 + s*U .. row0 + s*U + U - 1.
+// A "step" is U rows per slot (U * 64/LPR rows per wave) and U * GPL loads
+// per lane; slot s takes rows row0 + s*U .. row0 + s*U + U - 1.
+// Loads of 16 bytes per lane in one step (rows per slot = this / GPL, at
+// least one).  Six measured best on the 3B- and 8B-class decode steps: the
+// 8B step's K=4096 linears then take three rows per slot.
+#ifndef WQ_STEP_LOADS
+#define WQ_STEP_LOADS 6
+#endif
+
+__host__ __device__ constexpr int step_rows_per_slot(int gpl) {
+    return gpl >= WQ_STEP_LOADS ? 1 : WQ_STEP_LOADS / gpl;
+}
+
 template <int LPR, int GPL>
 struct StepShape {
     static constexpr int SLOTS = kWave / LPR;
-    static constexpr int U = GPL >= 8 ? 1 : 8 / GPL;  // rows per slot
-    static constexpr int ROWS = U * SLOTS;            // rows per step
+    static constexpr int U = step_rows_per_slot(GPL);  // rows per slot
+    static constexpr int ROWS = U * SLOTS;             // rows per step
 };
 
 // One step's loads: per row and group, the 16-byte group of codes and its
 // 2-byte scale.
 struct StepBuf {
-    u32x4 w[8];
-    uint32_t s[8];
+    u32x4 w[WQ_STEP_LOADS > 8 ? WQ_STEP_LOADS : 8];
+    uint32_t s[WQ_STEP_LOADS > 8 ? WQ_STEP_LOADS : 8];
 };
 
 // Orders one wave's LDS accesses across its lanes: a wave's LDS operations
@@ -237,7 +248,8 @@ __device__ __forceinline__ void compute_step(const StepBuf& b, const half2v (&xr
 }
 
 // Rows of y a wave stages in LDS before writing them out (2 KiB per wave).
-// Every rows-per-step value divides it.
+// Launches and plans cap a wave's rows at the largest multiple of its rows
+// per step that fits.
 constexpr int kYRows = 1024;
 
 // Write the `count` staged rows ylds[0, count) to y[row0, row0 + count),
