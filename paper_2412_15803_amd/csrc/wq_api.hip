@@ -117,8 +117,8 @@ class SpanSet {
 // Split the linears into consecutive groups in which no linear reads the
 // output of, or writes the input or output of, another linear of the same
 // group.  Groups run in stream order, so this reproduces running the linears
-// one after another.  Linears the grouped kernel cannot take (K > 16384) form
-// groups of their own.
+// one after another.  Linears the grouped kernel cannot take (K > 16384, or
+// codes of 4 GiB or more) form groups of their own.
 struct Group {
     int begin, end;  // linear indices [begin, end)
     bool grouped;    // run with the grouped kernel (else one GEMV launch)
@@ -131,7 +131,7 @@ std::vector<Group> split_groups(const std::vector<wq_linear>& lin) {
     int begin = 0;
     for (int i = 0; i < count; ++i) {
         const wq_linear& l = lin[i];
-        if (l.K / 32 > 64 * wq::kDecodeMaxGpl) {
+        if (l.K / 32 > 64 * wq::kDecodeMaxGpl || !wq::dev::fits_rsrc(l.N, l.K / 32)) {
             if (i > begin) groups.push_back(Group{begin, i, true});
             groups.push_back(Group{i, i + 1, false});
             reads.clear();
@@ -321,8 +321,8 @@ wq_status decode_per_linear(const char* fn, const wq_linear* lin, int64_t count,
     return WQ_OK;
 }
 
-// M = 1: one grouped launch per dependency group (one GEMV launch for
-// linears with K > 16384), all on `stream`.
+// M = 1: one grouped launch per dependency group (one GEMV launch for the
+// linears the grouped kernel cannot take), all on `stream`.
 wq_status decode_grouped(const char* fn, const std::vector<wq_linear>& lin, hipStream_t stream) {
     const std::vector<Group> groups = split_groups(lin);
     std::lock_guard<std::mutex> guard(g_ws_mu);

@@ -32,11 +32,10 @@ struct Step {
     int lin;                 // -1 past the end of the wave's range
     int nrows;               // rows of this step inside its linear
     int ng;
+    uint32_t scale_bytes;    // n * ng * 2: extent of the scales (codes: 8x)
     int64_t row;             // first row
-    const u32x4* packed;
+    const void* packed;
     const uint16_t* scales;
-    const uint16_t* x;
-    uint16_t* y;
 };
 
 // Walks the wave's step range [pos, end) of a class: steps are numbered per
@@ -57,11 +56,10 @@ __device__ __forceinline__ void load_linear(StepIter& it, const DecodePlan& p, c
     const DecodeEntry& e = p.entries[lin];
     it.cur.lin = lin;
     it.cur.ng = e.ng;
-    it.cur.row = e.n;  // rows of the linear, kept here for the clamp
-    it.cur.packed = reinterpret_cast<const u32x4*>(e.packed);
+    it.cur.row = e.n;  // rows of the linear, for the last step's row count
+    it.cur.packed = e.packed;
     it.cur.scales = e.scales;
-    it.cur.x = e.x;
-    it.cur.y = e.y;
+    it.cur.scale_bytes = (uint32_t)(e.n * e.ng * 2);
     it.first_step = e.first_step;
     it.lin_end = e.first_step + e.steps;
 }
@@ -98,15 +96,18 @@ struct XSlot {
     int64_t ybase, yend;
 };
 
+// x and y of the linear a step belongs to are read from the plan only when
+// the wave enters that linear.
 template <int LPR, int GPL, int MAXG>
-__device__ __forceinline__ void compute_from(const StepBuf& b, XSlot<MAXG>& xs, const Step& s, uint16_t* ylds,
-                                             int lane) {
+__device__ __forceinline__ void compute_from(const StepBuf& b, XSlot<MAXG>& xs, const Step& s,
+                                             const DecodePlan& p, uint16_t* ylds, int lane) {
     if (s.lin < 0) return;
     if (xs.lin != s.lin) {
         if (xs.lin >= 0) flush_y(xs.y, xs.ybase, ylds, (int)(xs.yend - xs.ybase), lane);
-        load_x_lane<LPR, GPL, MAXG>(s.x, s.ng, lane, xs.xr);
+        const DecodeEntry& e = p.entries[s.lin];
+        load_x_lane<LPR, GPL, MAXG>(e.x, s.ng, lane, xs.xr);
         xs.lin = s.lin;
-        xs.y = s.y;
+        xs.y = e.y;
         xs.ybase = s.row;
     }
     compute_step<LPR, GPL, MAXG>(b, xs.xr, s.nrows, ylds, (int)(s.row - xs.ybase), lane);
@@ -118,7 +119,7 @@ __device__ __forceinline__ void compute_from(const StepBuf& b, XSlot<MAXG>& xs, 
 // the same loads and the compiler's wait counts stay exact.
 template <int LPR, int GPL>
 __device__ __forceinline__ void issue_from(StepBuf& b, const Step& s, int lane) {
-    issue_step<LPR, GPL>(b, s.packed, s.scales, s.row, s.row + s.nrows - 1, s.ng, lane);
+    issue_step<LPR, GPL>(b, make_rsrc(s.packed, s.scales, s.scale_bytes), s.row, s.ng, lane);
 }
 
 // Register buffers in the pipeline: as many steps as fit a budget of
@@ -171,7 +172,7 @@ __device__ __forceinline__ void run_range(const DecodePlan& p, const DecodeClass
         bool any = false;
 #pragma unroll
         for (int i = 0; i < NB; ++i) {
-            compute_from<LPR, GPL, MAXG>(buf[i], xs, st[i], ylds, lane);
+            compute_from<LPR, GPL, MAXG>(buf[i], xs, st[i], p, ylds, lane);
             st[i] = next_step<R>(it, p, c);
             if (st[i].lin >= 0) last = st[i];
             any = any || st[i].lin >= 0;

@@ -190,35 +190,61 @@ __device__ __forceinline__ void load_x_lane(const uint16_t* x, int ng, int lane,
     }
 }
 
-// Issue the loads of rows [row0, row0 + ROWS) (clamped to last_row, so every
-// lane always loads a valid address and no branch is needed).
+// Buffer resources over one linear's codes and scales.  A load's byte offset
+// is this lane's offset within a step (the same vector register for every
+// step) plus a wave-uniform scalar offset for the step, row and group, so
+// issuing a step costs no vector address arithmetic.  The range check covers
+// the sum (checked on the device: a read whose scalar offset alone passes the
+// end returns zeros), so the rows past N in a linear's last step read zeros
+// and nothing out of bounds.  Offsets are 32-bit: a linear is read this way
+// only when its codes fit in 4 GiB (the launchers check).
+struct LinearRsrc {
+    __amdgpu_buffer_rsrc_t w;  // codes, n * ng * 16 bytes
+    __amdgpu_buffer_rsrc_t s;  // scales, n * ng * 2 bytes
+};
+
+constexpr int kRawBufferFlags = 0x00020000;  // word 3 of a raw (unswizzled) gfx9 buffer resource
+
+// From the two base pointers and the scales' size in bytes (n * ng * 2; the
+// codes take eight times that).
+__device__ __forceinline__ LinearRsrc make_rsrc(const void* packed, const uint16_t* scales, uint32_t scale_bytes) {
+    LinearRsrc r;
+    r.w = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(packed), (short)0, (int)(scale_bytes * 8u),
+                                            kRawBufferFlags);
+    r.s = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(scales), (short)0, (int)scale_bytes,
+                                            kRawBufferFlags);
+    return r;
+}
+
+// Issue the loads of rows [row0, row0 + ROWS) of a linear with ng groups per
+// row.  Lanes whose group index runs past the row read the next row's codes
+// (or zeros at the end); their x is zero, so those codes add nothing.
 template <int LPR, int GPL>
-__device__ __forceinline__ void issue_step(StepBuf& b, const u32x4* packed, const uint16_t* scales,
-                                           int64_t row0, int64_t last_row, int ng, int lane) {
+__device__ __forceinline__ void issue_step(StepBuf& b, const LinearRsrc& r, int64_t row0, int ng, int lane) {
     using S = StepShape<LPR, GPL>;
     const int slot = lane / LPR;
     const int sub = lane & (LPR - 1);
-    const WQ_GLOBAL u32x4* gp = gbl(packed);
-    const WQ_GLOBAL uint16_t* gs = gbl(scales);
+    // This lane's group index relative to the step's first group.
+    const uint32_t lg = (uint32_t)(slot * S::U * ng + sub);
+    const uint32_t g0 = (uint32_t)(row0 * ng);  // wave-uniform
 #pragma unroll
     for (int u = 0; u < S::U; ++u) {
-        const int64_t r = min(row0 + slot * S::U + u, last_row);
 #pragma unroll
         for (int j = 0; j < GPL; ++j) {
-            const int g = min(sub + LPR * j, ng - 1);
-            const int64_t idx = r * ng + g;
-            b.w[u * GPL + j] = gp[idx];
-            b.s[u * GPL + j] = gs[idx];
+            const uint32_t go = g0 + (uint32_t)(u * ng + LPR * j);  // wave-uniform
+            b.w[u * GPL + j] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r.w, lg * 16, go * 16, 0));
+            b.s[u * GPL + j] = __builtin_amdgcn_raw_buffer_load_b16(r.s, lg * 2, go * 2, 0);
         }
     }
     // Keep this step's loads ahead of anything issued later: the load counter
     // retires in issue order, so a later step's loads must not be scheduled
-    // in between, or waiting for this step would wait for those too.  The asm
-    // statement stops IR-level motion (the weight pointers are deliberately
-    // not __restrict__, so it binds them), the builtin the machine scheduler.
+    // in between, or waiting for this step would wait for those too.
     asm volatile("" ::: "memory");
     __builtin_amdgcn_sched_barrier(0);
 }
+
+// Whether a linear's codes can be addressed through 32-bit buffer offsets.
+__host__ __device__ inline bool fits_rsrc(int64_t n, int64_t ng) { return n * ng * 16 <= 0xFFFFFFFFll; }
 
 // Dot products, segment reduction and fp16 rounding of one step; the rows
 // below nrows are staged in this wave's LDS slice at ylds[yrel + row], to be

@@ -79,8 +79,8 @@ __global__ __launch_bounds__(kBlock) void gemv_m1_kernel(const u32x4* packed, co
     const int64_t rb = wave * rows_per_wave;
     if (rb >= n) return;
     const int64_t re = min(n, rb + rows_per_wave);
-    const int64_t last = re - 1;
     const int64_t steps = (re - rb + R - 1) / R;
+    const LinearRsrc rs = make_rsrc(packed, scales, (uint32_t)(n * ng * 2));
 
     __shared__ __align__(16) uint16_t s_y[kWavesPerBlock][kYRows];
     uint16_t* ylds = s_y[threadIdx.x / kWave];
@@ -90,18 +90,18 @@ __global__ __launch_bounds__(kBlock) void gemv_m1_kernel(const u32x4* packed, co
 
     // The loop starts two steps early so that the first pass only issues and
     // every load comes from the same two issue sites (one register
-    // assignment, no prologue copies that would force a full wait).  Loads
-    // past the wave's rows are clamped to its last row, so every issue is
-    // unconditional and the wait counts stay exact.
+    // assignment, no prologue copies that would force a full wait).  Every
+    // issue is unconditional (past the matrix the loads read zeros), so the
+    // wait counts stay exact.
     StepBuf a, b;
     for (int64_t s = -2; s < steps; s += 2) {
         const int64_t ra = rb + s * R;
         if (s >= 0) compute_step<LPR, GPL, GPL>(a, xr, (int)min((int64_t)R, re - ra), ylds, (int)(s * R), lane);
-        issue_step<LPR, GPL>(a, packed, scales, ra + 2 * R, last, ng, lane);
+        issue_step<LPR, GPL>(a, rs, ra + 2 * R, ng, lane);
         const int64_t rbb = ra + R;
         if (s + 1 >= 0 && s + 1 < steps)
             compute_step<LPR, GPL, GPL>(b, xr, (int)min((int64_t)R, re - rbb), ylds, (int)((s + 1) * R), lane);
-        issue_step<LPR, GPL>(b, packed, scales, rbb + 2 * R, last, ng, lane);
+        issue_step<LPR, GPL>(b, rs, rbb + 2 * R, ng, lane);
     }
     flush_y(y, rb, ylds, (int)(re - rb), lane);
 }
@@ -180,7 +180,7 @@ hipError_t launch_pack(const float* w, uint32_t* packed, uint16_t* scales, int64
 hipError_t launch_gemv(const uint32_t* packed, const uint16_t* scales, const uint16_t* x, uint16_t* y,
                        int64_t n, int64_t k, int64_t m, hipStream_t stream) {
     const int64_t ng = k / kGroup;
-    if (m == 1 && ng <= 512) {
+    if (m == 1 && ng <= 512 && fits_rsrc(n, ng)) {
         int lpr = 64, gpl = 1;
         pick_shape((int)ng, lpr, gpl);
 #define WQ_M1_CASE(L, G) \
