@@ -191,7 +191,7 @@ hipError_t launch_gemv(const uint32_t* packed, const uint16_t* scales, const uin
         WQ_M1_CASE(16, 1) WQ_M1_CASE(16, 3) WQ_M1_CASE(16, 5) WQ_M1_CASE(16, 7)
 #undef WQ_M1_CASE
     }
-    if (m >= 2 && m <= 64) return launch_gemm_mfma(packed, scales, x, y, n, k, m, stream);
+    if (m >= 2 && m <= 64 && fits_rsrc(n, ng)) return launch_gemm_mfma(packed, scales, x, y, n, k, m, stream);
     constexpr int MC = 4;
     const int64_t mchunks = (m + MC - 1) / MC;
     const int64_t waves = n * mchunks;

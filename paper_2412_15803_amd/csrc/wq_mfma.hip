@@ -38,14 +38,11 @@ using namespace dev;
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float float4v __attribute__((ext_vector_type(4)));
 
-// One step's loads: per weight-row tile u, this lane's 16-byte group and its
-// scale; the four x pieces (one per group of the step) for this lane's batch
-// row and word.
-template <int U>
-struct MStep {
-    u32x4 w[U];
-    uint32_t s[U];
-    u32x4 xa[4];
+// One item's loads: this lane's 16-byte group of one weight-row tile at one
+// step, and its scale.
+struct MItem {
+    u32x4 w;
+    uint32_t s;
 };
 
 // Transpose 4 x 4 dwords held as register r in 16-lane row c (value M[c][r])
@@ -63,138 +60,149 @@ __device__ __forceinline__ void transpose4(uint32_t& a0, uint32_t& a1, uint32_t&
     a2 = q23[0]; a3 = q23[1];
 }
 
-// The unconditional loads of step `step` (groups 4 step .. 4 step + 3);
-// group and row indices are clamped, so every address is valid.
-template <int U>
-__device__ __forceinline__ void issue_mstep(MStep<U>& b, const u32x4* packed, const uint16_t* scales,
-                                            const uint16_t* xrow, const int64_t (&roff)[U], int step, int ng,
-                                            int c) {
-    const WQ_GLOBAL u32x4* gp = gbl(packed);
-    const WQ_GLOBAL uint16_t* gs = gbl(scales);
-    const int g = min(4 * step + c, ng - 1);
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-        b.w[u] = gp[roff[u] + g];
-        b.s[u] = gs[roff[u] + g];
-    }
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-        const int gt = min(4 * step + t, ng - 1);
-        b.xa[t] = *reinterpret_cast<const WQ_GLOBAL u32x4*>(gbl(xrow) + gt * kGroup + 8 * c);
-    }
+constexpr int kChunk = 4;   // steps of 4 groups whose x a wave holds at once
+constexpr int kDepth = 8;   // items in flight per wave
+
+// Issue item (tile tt, step s): rows row0 + 16 tt + (lane % 16), group
+// 4 s + lane / 16.  The scalar offset carries everything wave-uniform; rows
+// past N read zeros.
+__device__ __forceinline__ void issue_item(MItem& b, const LinearRsrc& r, uint32_t lg, int64_t row0, int tt, int s,
+                                           int ng) {
+    const uint32_t go = (uint32_t)((row0 + 16 * tt) * ng + 4 * s);
+    b.w = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r.w, lg * 16, go * 16, 0));
+    b.s = __builtin_amdgcn_raw_buffer_load_b16(r.s, lg * 2, go * 2, 0);
     asm volatile("" ::: "memory");
     __builtin_amdgcn_sched_barrier(0);
 }
 
-// Multiply-accumulate one step into acc[u] (16 batch rows x 16 weight rows).
-template <int U>
-__device__ __forceinline__ void compute_mstep(const MStep<U>& b, float4v (&acc)[U], int step, int ng, int c) {
-    // Operand A pieces: x[8c .. 8c + 8) of each group, reordered to the
-    // dequantized codes' order (0, 4), (1, 5), (2, 6), (3, 7).
-    half8 xa[4];
+// Multiply-accumulate one item into acc (16 batch rows x the tile's 16 weight
+// rows).  `valid`: the step lies in this wave's range and this lane's group
+// in the row; otherwise the scale is zero and the item adds nothing.
+__device__ __forceinline__ void compute_item(const MItem& b, const half8 (&xa)[4], float4v& acc, bool valid) {
+    uint32_t w0 = b.w.x, w1 = b.w.y, w2 = b.w.z, w3 = b.w.w;
+    transpose4(w0, w1, w2, w3);
+    uint32_t s0 = valid ? b.s : 0u;
+    uint32_t s1 = s0, s2 = s0, s3 = s0;
+    transpose4(s0, s1, s2, s3);
+    const uint32_t wt[4] = {w0, w1, w2, w3};
+    const uint32_t st[4] = {s0, s1, s2, s3};
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-        const u32x4 d = b.xa[t];
+        half2v q[4];
+        dequant_word(wt[t], q);
+        // (q - 8) * s rounded once to fp16: the group's weights in the scale
+        // of operand B, so the multiplies accumulate across groups.
+        const half2v sc = as_h2((st[t] & 0xFFFFu) | (st[t] << 16));
+        const u32x4 qb = {__builtin_bit_cast(uint32_t, q[0] * sc), __builtin_bit_cast(uint32_t, q[1] * sc),
+                          __builtin_bit_cast(uint32_t, q[2] * sc), __builtin_bit_cast(uint32_t, q[3] * sc)};
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(xa[t], __builtin_bit_cast(half8, qb), acc, 0, 0, 0);
+    }
+}
+
+// x for one step as operand A pieces: x[8c .. 8c + 8) of each of its four
+// groups for batch row lane % 16, reordered to the dequantized codes' order
+// (0, 4), (1, 5), (2, 6), (3, 7).  Groups past the row are clamped (their
+// weights are masked).
+__device__ __forceinline__ void load_x_step(const uint16_t* xrow, int s, int ng, int c, half8 (&xa)[4]) {
+    u32x4 d[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        const int g = min(4 * s + t, ng - 1);
+        d[t] = *reinterpret_cast<const WQ_GLOBAL u32x4*>(gbl(xrow) + g * kGroup + 8 * c);
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
         u32x4 r;
-        r.x = __builtin_amdgcn_perm(d.z, d.x, 0x05040100u);
-        r.y = __builtin_amdgcn_perm(d.z, d.x, 0x07060302u);
-        r.z = __builtin_amdgcn_perm(d.w, d.y, 0x05040100u);
-        r.w = __builtin_amdgcn_perm(d.w, d.y, 0x07060302u);
+        r.x = __builtin_amdgcn_perm(d[t].z, d[t].x, 0x05040100u);
+        r.y = __builtin_amdgcn_perm(d[t].z, d[t].x, 0x07060302u);
+        r.z = __builtin_amdgcn_perm(d[t].w, d[t].y, 0x05040100u);
+        r.w = __builtin_amdgcn_perm(d[t].w, d[t].y, 0x07060302u);
         xa[t] = __builtin_bit_cast(half8, r);
     }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-        uint32_t w0 = b.w[u].x, w1 = b.w[u].y, w2 = b.w[u].z, w3 = b.w[u].w;
-        transpose4(w0, w1, w2, w3);
-        // Scale of this lane's row for group 4 step + c; zero past the row's
-        // groups (the clamped codes then add nothing).
-        uint32_t s0 = 4 * step + c < ng ? b.s[u] : 0u;
-        uint32_t s1 = s0, s2 = s0, s3 = s0;
-        transpose4(s0, s1, s2, s3);
-        const uint32_t wt[4] = {w0, w1, w2, w3};
-        const uint32_t st[4] = {s0, s1, s2, s3};
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            half2v q[4];
-            dequant_word(wt[t], q);
-            // (q - 8) * s rounded once to fp16: the group's weights in the
-            // scale of operand B, so the multiplies accumulate across groups.
-            const uint32_t sp = (st[t] & 0xFFFFu) | (st[t] << 16);
-            const half2v sc = as_h2(sp);
-            const u32x4 qb = {__builtin_bit_cast(uint32_t, q[0] * sc), __builtin_bit_cast(uint32_t, q[1] * sc),
-                              __builtin_bit_cast(uint32_t, q[2] * sc), __builtin_bit_cast(uint32_t, q[3] * sc)};
-            acc[u] = __builtin_amdgcn_mfma_f32_16x16x32_f16(xa[t], __builtin_bit_cast(half8, qb), acc[u], 0, 0, 0);
-        }
-    }
 }
 
-template <int U, int W, int NB>
-__global__ __launch_bounds__(64 * W) void gemm_mfma_kernel(const u32x4* packed, const uint16_t* scales,
-                                                           const uint16_t* __restrict__ x,
-                                                           uint16_t* __restrict__ y, int64_t n, int ng, int m) {
+// A block owns T tiles of 16 weight rows; its waves (blockDim / 64 of them)
+// split the row's steps into contiguous ranges.  A wave takes its range in
+// chunks of kChunk steps: it loads the chunk's x once, then streams every
+// tile's codes for those steps through a kDepth-item register pipeline.  The
+// waves' partial tiles are summed through LDS in a fixed order.
+template <int T>
+__global__ __launch_bounds__(512) void gemm_mfma_kernel(const void* packed, const uint16_t* scales,
+                                                        const uint16_t* __restrict__ x, uint16_t* __restrict__ y,
+                                                        int64_t n, int ng, int m) {
+    constexpr int kItems = T * kChunk;
+    constexpr int kPre = kDepth < kItems ? kDepth : kItems;
     const int lane = threadIdx.x & (kWave - 1);
+    const int nw = blockDim.x / kWave;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int li = lane & 15, c = lane >> 4;
-    const int64_t row0 = (int64_t)blockIdx.x * 16 * U;
-    int64_t roff[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) roff[u] = min(row0 + 16 * u + li, n - 1) * ng;
-    const uint16_t* xrow = x + (int64_t)min(li, m - 1) * ng * kGroup;
+    const int64_t row0 = (int64_t)blockIdx.x * 16 * T;
     const int nsteps = (ng + 3) / 4;
-    const int sb = wave * nsteps / W, se = (wave + 1) * nsteps / W;
+    const int sb = wave * nsteps / nw, se = (wave + 1) * nsteps / nw;
+    const LinearRsrc rs = make_rsrc(packed, scales, (uint32_t)(n * ng * 2));
+    const uint32_t lg = (uint32_t)(li * ng + c);
+    const uint16_t* xrow = x + (int64_t)min(li, m - 1) * ng * kGroup;
 
-    float4v acc[U];
+    float4v acc[T];
 #pragma unroll
-    for (int u = 0; u < U; ++u) acc[u] = float4v{0.0f, 0.0f, 0.0f, 0.0f};
-    // Same loop shape as the batch-1 kernels: NB register buffers, starting
-    // NB steps early so the first pass only issues; loads past the range
-    // re-read its last step.
-    MStep<U> buf[NB];
-    const int last = max(se - 1, sb);
-    for (int s = sb - NB; s < se; s += NB) {
+    for (int tt = 0; tt < T; ++tt) acc[tt] = float4v{0.0f, 0.0f, 0.0f, 0.0f};
+
+    for (int c0 = sb; c0 < se; c0 += kChunk) {
+        MItem buf[kPre];
 #pragma unroll
-        for (int i = 0; i < NB; ++i) {
-            if (s + i >= sb && s + i < se) compute_mstep<U>(buf[i], acc, s + i, ng, c);
-            issue_mstep<U>(buf[i], packed, scales, xrow, roff, min(s + i + NB, last), ng, c);
+        for (int q = 0; q < kPre; ++q) issue_item(buf[q], rs, lg, row0, q / kChunk, c0 + q % kChunk, ng);
+        half8 xa[kChunk][4];
+#pragma unroll
+        for (int k = 0; k < kChunk; ++k) load_x_step(xrow, min(c0 + k, nsteps - 1), ng, c, xa[k]);
+#pragma unroll
+        for (int q = 0; q < kItems; ++q) {
+            const int tt = q / kChunk, k = q % kChunk, s = c0 + k;
+            compute_item(buf[q % kPre], xa[k], acc[tt], s < se && 4 * s + c < ng);
+            if (q + kPre < kItems)
+                issue_item(buf[q % kPre], rs, lg, row0, (q + kPre) / kChunk, c0 + (q + kPre) % kChunk, ng);
         }
     }
 
-    // Sum the W waves' partial tiles; wave 0 rounds and stores.
-    __shared__ float red[W > 1 ? W : 1][U][4][kWave];
-    if constexpr (W > 1) {
+    // Sum the waves' partial tiles in wave order; one wave per tile rounds
+    // and stores it.
+    __shared__ float red[8][4][kWave];
+    for (int tt = 0; tt < T; ++tt) {
+        float4v mine = acc[0];
 #pragma unroll
-        for (int u = 0; u < U; ++u)
+        for (int u = 1; u < T; ++u)
+            if (u == tt) mine = acc[u];
+        if (nw > 1) {
 #pragma unroll
-            for (int v = 0; v < 4; ++v) red[wave][u][v][lane] = acc[u][v];
-        __syncthreads();
-        if (wave != 0) return;
+            for (int v = 0; v < 4; ++v) red[wave][v][lane] = mine[v];
+            __syncthreads();
+        }
+        if (wave == tt % nw) {
+            float4v tot = mine;
+            if (nw > 1) {
 #pragma unroll
-        for (int u = 0; u < U; ++u)
+                for (int v = 0; v < 4; ++v) {
+                    float t = 0.0f;
+                    for (int w = 0; w < nw; ++w) t += red[w][v][lane];
+                    tot[v] = t;
+                }
+            }
+            const int64_t col = row0 + 16 * tt + li;
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                float t = 0.0f;
-                for (int w = 0; w < W; ++w) t += red[w][u][v][lane];
-                acc[u][v] = t;
+                const int mr = 4 * c + v;
+                if (mr < m && col < n) gbl(y)[mr * n + col] = __half_as_ushort(__float2half_rn(tot[v]));
             }
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-        const int64_t col = row0 + 16 * u + li;
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int mr = 4 * c + v;
-            if (mr < m && col < n) gbl(y)[mr * n + col] = __half_as_ushort(__float2half_rn(acc[u][v]));
         }
+        if (nw > 1) __syncthreads();
     }
 }
 
-template <int U, int W>
-hipError_t launch_u_w(const uint32_t* packed, const uint16_t* scales, const uint16_t* x, uint16_t* y, int64_t n,
-                      int64_t ng, int m, hipStream_t stream) {
-    constexpr int NB = 3;
-    const int64_t blocks = (n + 16 * U - 1) / (16 * U);
-    hipLaunchKernelGGL((gemm_mfma_kernel<U, W, NB>), dim3((unsigned)blocks), dim3(64 * W), 0, stream,
-                       reinterpret_cast<const u32x4*>(packed), scales, x, y, n, (int)ng, m);
+template <int T>
+hipError_t launch_t(const uint32_t* packed, const uint16_t* scales, const uint16_t* x, uint16_t* y, int64_t n,
+                    int64_t ng, int m, int w, hipStream_t stream) {
+    const int64_t blocks = (n + 16 * T - 1) / (16 * T);
+    hipLaunchKernelGGL((gemm_mfma_kernel<T>), dim3((unsigned)blocks), dim3(64 * w), 0, stream, packed, scales, x, y,
+                       n, (int)ng, m);
     return hipGetLastError();
 }
 
@@ -204,27 +212,23 @@ hipError_t launch_gemm_mfma(const uint32_t* packed, const uint16_t* scales, cons
                             int64_t n, int64_t k, int64_t m, hipStream_t stream) {
     const int64_t ng = k / kGroup;
     const int64_t nsteps = (ng + 3) / 4;
-    // Row tiles per block: as many (up to 4) as still leave 512 blocks, so a
-    // wave's x loads serve several tiles; then waves per block (a split of
-    // the row's groups) up to about 1024 waves, each keeping at least three
-    // steps.  (Measured on the 8B shapes: more waves than that only add x
-    // traffic.)
-    int u = 4;
-    while (u > 1 && (n + 16 * u - 1) / (16 * u) < 512) u /= 2;
-    const int64_t blocks = (n + 16 * u - 1) / (16 * u);
-    int w = 1;
-    while (w < 16 && blocks * w * 2 <= 1024 && nsteps / (w * 2) >= 3) w *= 2;
+    // Waves per block: one chunk of steps each where K allows, at most 8.
+    const int w = (int)std::min<int64_t>(8, (nsteps + kChunk - 1) / kChunk);
+    // Tiles per block: as many (up to 8, sharing each x load) as still keep
+    // about 1536 waves in flight.
+    int t = 8;
+    while (t > 1 && (n + 16 * t - 1) / (16 * t) * w < 1536) t /= 2;
     for (int64_t m0 = 0; m0 < m; m0 += 16) {
         const int mc = (int)std::min<int64_t>(16, m - m0);
         const uint16_t* xc = x + m0 * k;
         uint16_t* yc = y + m0 * n;
         hipError_t e = hipSuccess;
-#define WQ_MFMA_CASE(U, W) \
-    if (u == U && w == W) e = launch_u_w<U, W>(packed, scales, xc, yc, n, ng, mc, stream);
-        WQ_MFMA_CASE(1, 1) WQ_MFMA_CASE(1, 2) WQ_MFMA_CASE(1, 4) WQ_MFMA_CASE(1, 8) WQ_MFMA_CASE(1, 16)
-        WQ_MFMA_CASE(2, 1) WQ_MFMA_CASE(2, 2) WQ_MFMA_CASE(2, 4) WQ_MFMA_CASE(2, 8) WQ_MFMA_CASE(2, 16)
-        WQ_MFMA_CASE(4, 1) WQ_MFMA_CASE(4, 2) WQ_MFMA_CASE(4, 4) WQ_MFMA_CASE(4, 8) WQ_MFMA_CASE(4, 16)
-#undef WQ_MFMA_CASE
+        switch (t) {
+            case 8: e = launch_t<8>(packed, scales, xc, yc, n, ng, mc, w, stream); break;
+            case 4: e = launch_t<4>(packed, scales, xc, yc, n, ng, mc, w, stream); break;
+            case 2: e = launch_t<2>(packed, scales, xc, yc, n, ng, mc, w, stream); break;
+            default: e = launch_t<1>(packed, scales, xc, yc, n, ng, mc, w, stream); break;
+        }
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
