@@ -89,18 +89,18 @@ def chained_step(lins):
     return out
 
 
-def time_steps(lins, arr, steps, warmup):
+def time_steps(lins, arr, steps, warmup, m=1):
     import torch
 
     from paper_2412_15803_amd import wq
 
     for _ in range(warmup):
-        wq.wq_decode_linears(lins, m=1, _array=arr)
+        wq.wq_decode_linears(lins, m=m, _array=arr)
     torch.cuda.synchronize()
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     start.record()
     for _ in range(steps):
-        wq.wq_decode_linears(lins, m=1, _array=arr)
+        wq.wq_decode_linears(lins, m=m, _array=arr)
     end.record()
     torch.cuda.synchronize()
     return start.elapsed_time(end) / steps
@@ -202,26 +202,30 @@ def time_gemv_rotated(n, k, ms_list, gen, device, calls=200, reps=5):
     return out
 
 
-def step_8b(gen, device, steps, warmup):
-    """The 8B-class decode step: 32 x (qkv 6144x4096, o 4096x4096, gate_up
-    28672x4096, down 4096x14336) + lm_head 128256x4096, random codes, M=1."""
+def time_step_batches(shapes, batches, gen, device, steps, warmup):
+    """One decode step of the given linear shapes (random codes), timed as one
+    wq_decode_linears call per step at each batch size M."""
     import torch
 
     from paper_2412_15803_amd import workloads as wl
     from paper_2412_15803_amd import wq
 
-    shapes = [(lin.n, lin.k) for lin in wl.LLAMA8B_LAYER] * 32 + [(128256, 4096)]
-    lins, total = [], 0
-    for n, k in shapes:
-        p, s = random_linear(n, k, gen, device)
-        x = torch.randn((1, k), device=device, generator=gen).to(torch.float16)
-        lins.append((p, s, x, torch.empty((1, n), dtype=torch.float16, device=device)))
-        total += wl.ideal_bytes(n, k, 1)
-    ms = time_steps(lins, wq.make_linear_array(lins, 1), steps, warmup)
-    del lins
+    ws = [random_linear(n, k, gen, device) for n, k in shapes]
+    out = {}
+    for m in batches:
+        lins, total = [], 0
+        for (n, k), (p, s) in zip(shapes, ws):
+            x = torch.randn((m, k), device=device, generator=gen).to(torch.float16)
+            lins.append((p, s, x, torch.empty((m, n), dtype=torch.float16, device=device)))
+            total += wl.ideal_bytes(n, k, m)
+        ms = time_steps(lins, wq.make_linear_array(lins, m), steps, warmup, m=m)
+        gbs = total / (ms * 1e-3) / 1e9
+        out[m] = {"us": round(ms * 1e3, 2), "GB_s": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4),
+                  "tokens_per_s": round(m / (ms * 1e-3), 1)}
+        del lins
+    del ws
     torch.cuda.empty_cache()
-    return {"linears": len(shapes), "bytes": total, "us": round(ms * 1e3, 2),
-            "GB_s": round(total / (ms * 1e-3) / 1e9, 1), "frac": round(total / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+    return out
 
 
 def per_config(device, seed):
@@ -243,7 +247,12 @@ def per_config(device, seed):
         for m, v in got.items():
             res[f"8B {lin.name} {lin.n}x{lin.k} M={m}"] = v
     res["unit"] = "[us per call, GB/s]"
-    res["8B step M=1 (one wq_decode_linears call, 129 linears)"] = step_8b(gen, device, 50, 5)
+    steps3 = [(lin.n, lin.k) for lin in wl.LLAMA3B_LAYER] * 28 + [(wl.LLAMA3B_LM_HEAD.n, wl.LLAMA3B_LM_HEAD.k)]
+    steps8 = [(lin.n, lin.k) for lin in wl.LLAMA8B_LAYER] * 32 + [(128256, 4096)]
+    for m, v in time_step_batches(steps3, [4, 16], gen, device, 20, 3).items():
+        res[f"3B step M={m} (one wq_decode_linears call, 113 linears)"] = v
+    for m, v in time_step_batches(steps8, [1, 4, 16], gen, device, 20, 3).items():
+        res[f"8B step M={m} (one wq_decode_linears call, 129 linears)"] = v
     return res
 
 

@@ -124,14 +124,15 @@ struct Group {
     bool grouped;    // run with the grouped kernel (else one GEMV launch)
 };
 
-std::vector<Group> split_groups(const std::vector<wq_linear>& lin) {
+std::vector<Group> split_groups(const std::vector<wq_linear>& lin, int64_t m) {
     std::vector<Group> groups;
     SpanSet reads, writes;
     const int count = (int)lin.size();
     int begin = 0;
     for (int i = 0; i < count; ++i) {
         const wq_linear& l = lin[i];
-        if (l.K / 32 > 64 * wq::kDecodeMaxGpl || !wq::dev::fits_rsrc(l.N, l.K / 32)) {
+        const bool too_long = m == 1 && l.K / 32 > 64 * wq::kDecodeMaxGpl;
+        if (too_long || !wq::dev::fits_rsrc(l.N, l.K / 32)) {
             if (i > begin) groups.push_back(Group{begin, i, true});
             groups.push_back(Group{i, i + 1, false});
             reads.clear();
@@ -139,7 +140,7 @@ std::vector<Group> split_groups(const std::vector<wq_linear>& lin) {
             begin = i + 1;
             continue;
         }
-        const Span x = span_of(l.x, 2 * l.K), y = span_of(l.y, 2 * l.N);
+        const Span x = span_of(l.x, 2 * m * l.K), y = span_of(l.y, 2 * m * l.N);
         if (i > begin && (writes.hits(x) || reads.hits(y) || writes.hits(y))) {
             groups.push_back(Group{begin, i, true});
             reads.clear();
@@ -324,7 +325,7 @@ wq_status decode_per_linear(const char* fn, const wq_linear* lin, int64_t count,
 // M = 1: one grouped launch per dependency group (one GEMV launch for the
 // linears the grouped kernel cannot take), all on `stream`.
 wq_status decode_grouped(const char* fn, const std::vector<wq_linear>& lin, hipStream_t stream) {
-    const std::vector<Group> groups = split_groups(lin);
+    const std::vector<Group> groups = split_groups(lin, 1);
     std::lock_guard<std::mutex> guard(g_ws_mu);
     DecodeWorkspace* ws = nullptr;
     wq_status st = get_workspace(fn, stream, ws);
@@ -347,6 +348,74 @@ wq_status decode_grouped(const char* fn, const std::vector<wq_linear>& lin, hipS
         p.class_lin = reinterpret_cast<const int32_t*>(ws->d_plan + gp.off_list);
         p.nclasses = gp.nclasses;
         if ((st = hip_status(fn, wq::launch_grouped_m1(p, gp.max_gpl, gp.waves, stream))) != WQ_OK) return st;
+    }
+    return WQ_OK;
+}
+// Plan of one small-batch grouped launch: the entries, each owning a run of
+// blocks (tiles of grouped_mfma_tiles() x 16 rows) of the grid.
+struct BatchPlan {
+    size_t off_entries;
+    int count;
+    int64_t blocks;
+    int waves_per_block;
+};
+
+BatchPlan plan_batch_group(const std::vector<wq_linear>& lin, const Group& g, std::vector<unsigned char>& bytes) {
+    const int count = g.end - g.begin;
+    const int rows_per_block = 16 * wq::grouped_mfma_tiles();
+    std::vector<wq::DecodeEntry> ents(count, wq::DecodeEntry{});
+    int64_t blocks = 0, max_steps = 1;
+    for (int i = 0; i < count; ++i) {
+        const wq_linear& l = lin[g.begin + i];
+        wq::DecodeEntry& e = ents[i];
+        e.packed = l.packed_w;
+        e.scales = l.scales;
+        e.x = l.x;
+        e.y = l.y;
+        e.n = l.N;
+        e.ng = (int32_t)(l.K / 32);
+        e.first_step = blocks;
+        e.steps = (l.N + rows_per_block - 1) / rows_per_block;
+        blocks += e.steps;
+        max_steps = std::max<int64_t>(max_steps, (e.ng + 3) / 4);
+    }
+    BatchPlan bp;
+    bp.count = count;
+    bp.blocks = blocks;
+    // About 32 steps of the longest row per wave (measured on the 3B- and
+    // 8B-class steps: fewer, longer waves keep more blocks resident per CU).
+    bp.waves_per_block = (int)std::min<int64_t>(8, (max_steps + 31) / 32);
+    bp.off_entries = align16(bytes.size());
+    bytes.resize(align16(bp.off_entries + sizeof(wq::DecodeEntry) * count), 0);
+    std::memcpy(bytes.data() + bp.off_entries, ents.data(), sizeof(wq::DecodeEntry) * count);
+    return bp;
+}
+
+// M >= 2: one matrix-core launch per dependency group and 16 batch rows.
+wq_status decode_grouped_batch(const char* fn, const std::vector<wq_linear>& lin, int64_t m, hipStream_t stream) {
+    const std::vector<Group> groups = split_groups(lin, m);
+    std::lock_guard<std::mutex> guard(g_ws_mu);
+    DecodeWorkspace* ws = nullptr;
+    wq_status st = get_workspace(fn, stream, ws);
+    if (st != WQ_OK) return st;
+    std::vector<unsigned char> bytes;
+    std::vector<BatchPlan> plans(groups.size());
+    for (size_t i = 0; i < groups.size(); ++i)
+        if (groups[i].grouped) plans[i] = plan_batch_group(lin, groups[i], bytes);
+    if (!bytes.empty() && (st = upload_plan(fn, ws, bytes, stream)) != WQ_OK) return st;
+    for (size_t i = 0; i < groups.size(); ++i) {
+        const Group& g = groups[i];
+        if (!g.grouped) {
+            if ((st = decode_per_linear(fn, &lin[g.begin], g.end - g.begin, m, stream)) != WQ_OK) return st;
+            continue;
+        }
+        const BatchPlan& bp = plans[i];
+        const wq::DecodeEntry* ents = reinterpret_cast<const wq::DecodeEntry*>(ws->d_plan + bp.off_entries);
+        for (int64_t m0 = 0; m0 < m; m0 += 16) {
+            const int mc = (int)std::min<int64_t>(16, m - m0);
+            st = hip_status(fn, wq::launch_grouped_mfma(ents, bp.count, bp.blocks, bp.waves_per_block, m0, mc, stream));
+            if (st != WQ_OK) return st;
+        }
     }
     return WQ_OK;
 }
@@ -434,7 +503,8 @@ wq_status wq_decode_linears(const wq_linear* linears, int64_t count, int64_t M, 
     (void)hipGetLastError();
     const hipStream_t s = static_cast<hipStream_t>(stream);
     if (M == 1) return decode_grouped(fn, lin, s);
-    // Batches: one launch per linear, in stream order.
+    if (M <= 64) return decode_grouped_batch(fn, lin, M, s);
+    // Larger batches: one launch per linear, in stream order.
     return decode_per_linear(fn, lin.data(), count, M, s);
 }
 

@@ -59,6 +59,14 @@ struct DecodePlan {
     int32_t nclasses;
 };
 
+// Small-batch decode step: independent linears in one launch of the matrix-core
+// kernel.  Entry i owns blocks [first_step, first_step + steps) of the grid,
+// each block grouped_mfma_tiles() tiles of 16 rows, waves_per_block <= 8;
+// batch rows [m0, m0 + m), m <= 16.
+int grouped_mfma_tiles();
+hipError_t launch_grouped_mfma(const DecodeEntry* entries, int count, int64_t blocks, int waves_per_block,
+                               int64_t m0, int m, hipStream_t stream);
+
 // Largest groups-per-lane of the grouped kernel (K <= 16384).
 constexpr int kDecodeMaxGpl = 8;
 constexpr int kMaxClasses = 16;

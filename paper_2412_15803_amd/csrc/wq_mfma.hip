@@ -121,22 +121,21 @@ __device__ __forceinline__ void load_x_step(const uint16_t* xrow, int s, int ng,
     }
 }
 
-// A block owns T tiles of 16 weight rows; its waves (blockDim / 64 of them)
-// split the row's steps into contiguous ranges.  A wave takes its range in
-// chunks of kChunk steps: it loads the chunk's x once, then streams every
-// tile's codes for those steps through a kDepth-item register pipeline.  The
-// waves' partial tiles are summed through LDS in a fixed order.
+// A block owns T tiles of 16 weight rows from row0 of one linear; its waves
+// (blockDim / 64 of them) split the row's steps into contiguous ranges.  A
+// wave takes its range in chunks of kChunk steps: it loads the chunk's x
+// once, then streams every tile's codes for those steps through a
+// kDepth-item register pipeline.  The waves' partial tiles are summed through
+// LDS in a fixed order and one wave per tile rounds and stores it.
 template <int T>
-__global__ __launch_bounds__(512) void gemm_mfma_kernel(const void* packed, const uint16_t* scales,
-                                                        const uint16_t* __restrict__ x, uint16_t* __restrict__ y,
-                                                        int64_t n, int ng, int m) {
+__device__ __forceinline__ void mfma_block(const void* packed, const uint16_t* scales, const uint16_t* x,
+                                           uint16_t* y, int64_t n, int ng, int m, int64_t row0) {
     constexpr int kItems = T * kChunk;
     constexpr int kPre = kDepth < kItems ? kDepth : kItems;
     const int lane = threadIdx.x & (kWave - 1);
     const int nw = blockDim.x / kWave;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int li = lane & 15, c = lane >> 4;
-    const int64_t row0 = (int64_t)blockIdx.x * 16 * T;
     const int nsteps = (ng + 3) / 4;
     const int sb = wave * nsteps / nw, se = (wave + 1) * nsteps / nw;
     const LinearRsrc rs = make_rsrc(packed, scales, (uint32_t)(n * ng * 2));
@@ -163,8 +162,6 @@ __global__ __launch_bounds__(512) void gemm_mfma_kernel(const void* packed, cons
         }
     }
 
-    // Sum the waves' partial tiles in wave order; one wave per tile rounds
-    // and stores it.
     __shared__ float red[8][4][kWave];
     for (int tt = 0; tt < T; ++tt) {
         float4v mine = acc[0];
@@ -197,6 +194,33 @@ __global__ __launch_bounds__(512) void gemm_mfma_kernel(const void* packed, cons
     }
 }
 
+// One linear: block b owns rows [16 T b, 16 T (b + 1)).
+template <int T>
+__global__ __launch_bounds__(512) void gemm_mfma_kernel(const void* packed, const uint16_t* scales,
+                                                        const uint16_t* __restrict__ x, uint16_t* __restrict__ y,
+                                                        int64_t n, int ng, int m) {
+    mfma_block<T>(packed, scales, x, y, n, ng, m, (int64_t)blockIdx.x * 16 * T);
+}
+
+// Independent linears of a decode step in one launch: entry i owns blocks
+// [first_step, first_step + steps) (its rows in 16 T-row tiles), found by
+// binary search; batch rows [m0, m0 + m) of every linear.
+template <int T>
+__global__ __launch_bounds__(512) void grouped_mfma_kernel(const DecodeEntry* __restrict__ entries, int count,
+                                                           int64_t m0, int m) {
+    const int64_t b = blockIdx.x;
+    int lo = 0, hi = count - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) / 2;
+        if (entries[mid].first_step <= b) lo = mid;
+        else hi = mid - 1;
+    }
+    const DecodeEntry& e = entries[lo];
+    const int64_t k = (int64_t)e.ng * kGroup;
+    mfma_block<T>(e.packed, e.scales, e.x + m0 * k, e.y + m0 * e.n, e.n, e.ng, m,
+                  (b - e.first_step) * 16 * T);
+}
+
 template <int T>
 hipError_t launch_t(const uint32_t* packed, const uint16_t* scales, const uint16_t* x, uint16_t* y, int64_t n,
                     int64_t ng, int m, int w, hipStream_t stream) {
@@ -207,6 +231,15 @@ hipError_t launch_t(const uint32_t* packed, const uint16_t* scales, const uint16
 }
 
 }  // namespace
+
+int grouped_mfma_tiles() { return 8; }
+
+hipError_t launch_grouped_mfma(const DecodeEntry* entries, int count, int64_t blocks, int waves_per_block,
+                               int64_t m0, int m, hipStream_t stream) {
+    hipLaunchKernelGGL((grouped_mfma_kernel<8>), dim3((unsigned)blocks), dim3(64 * waves_per_block), 0, stream,
+                       entries, count, m0, m);
+    return hipGetLastError();
+}
 
 hipError_t launch_gemm_mfma(const uint32_t* packed, const uint16_t* scales, const uint16_t* x, uint16_t* y,
                             int64_t n, int64_t k, int64_t m, hipStream_t stream) {

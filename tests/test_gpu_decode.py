@@ -1,5 +1,6 @@
-"""wq_decode_linears on the GPU: the persistent decode-step kernel (M = 1,
-K <= 16384) and the per-linear fallback, against the CPU oracle.
+"""wq_decode_linears on the GPU: the grouped batch-1 kernel (M = 1,
+K <= 16384), the grouped matrix-core kernel (2 <= M <= 64) and the
+per-linear fallback, against the CPU oracle.
 
 Outputs are pre-filled with NaN and every row is checked, so a tile that is
 never computed shows up.  Integer-valued data (unit scales, codes in
@@ -217,7 +218,8 @@ def test_many_linears_grow_workspace():
 
 
 def test_fallback_paths_small_batch_and_long_k():
-    """M > 1 and K > 16384 run as one launch per linear, still in order."""
+    """A two-linear chain at M = 4 (two grouped launches) and K > 16384 at
+    M = 1 (one launch per linear), still in order."""
     rng = np.random.default_rng(8)
     announce("decode fallback M=4 chain and K=16416")
     m = 4
@@ -263,3 +265,64 @@ def test_decode_matches_single_gemv_random_data():
         ok = oracle.within_tolerance(to_host(lin[3], np.float16), oracle.gemv(p, s, x, n, k),
                                      oracle.tol_bound(p, s, x, n, k))
         assert ok.all(), f"{n}x{k}"
+
+
+@pytest.mark.parametrize("m", [2, 4, 16, 17, 33])
+def test_small_batch_independent_linears_bit_exact(m):
+    """Independent linears of mixed K (a group count that is not a multiple
+    of 4, the 8B shapes' widths, K = 14336) and ragged N in one grouped
+    matrix-core launch per 16 batch rows; every row checked."""
+    rng = np.random.default_rng(100 + m)
+    shapes = [(300, 1056), (4096, 4096), (1000, 14336), (37, 800), (6144, 4096), (257, 2080)]
+    announce(f"decode small batch M={m}, {len(shapes)} independent linears")
+    host, lins = [], []
+    for n, k in shapes:
+        p, s = int_linear(rng, n, k, 1 / 8)
+        x = rng.integers(-1, 2, size=(m, k)).astype(np.float16)
+        host.append((p, s, x))
+        lins.append((to_dev(p), to_dev(s), to_dev(x), nan_out(m, n)))
+    run(lins, m=m)
+    for (p, s, x), lin, (n, k) in zip(host, lins, shapes):
+        check_exact(lin[3], oracle.gemv(p, s, x, n, k), f"M={m} {n}x{k}")
+
+
+@pytest.mark.parametrize("m", [4, 16])
+def test_small_batch_dependency_chain_bit_exact(m):
+    """x of linear i+1 is y of linear i for 12 linears: every linear is its
+    own grouped launch, in stream order."""
+    rng = np.random.default_rng(200 + m)
+    dims = [int(d) for d in rng.choice([256, 512, 1024, 2048], size=13)]
+    layers = [int_linear(rng, dims[i + 1], dims[i], 1 / 16) for i in range(12)]
+    x0 = rng.integers(-1, 2, size=(m, dims[0])).astype(np.float16)
+    announce(f"decode small batch M={m}, 12-linear chain")
+    lins, x = [], to_dev(x0)
+    for p, s in layers:
+        y = nan_out(m, p.shape[0])
+        lins.append((to_dev(p), to_dev(s), x, y))
+        x = y
+    run(lins, m=m)
+    xr = x0
+    for i, ((p, s), lin) in enumerate(zip(layers, lins)):
+        xr = oracle.gemv(p, s, xr, p.shape[0], p.shape[1] * 8)
+        check_exact(lin[3], xr, f"M={m} chain linear {i}")
+
+
+@pytest.mark.parametrize("m", [4, 16])
+def test_small_batch_decode_random_data_tolerance(m):
+    """Random codes, scales and x on the 8B layer's shapes: every output of
+    the grouped launch within tolerance of the oracle (sampled rows)."""
+    shapes = [(6144, 4096), (4096, 4096), (28672, 4096), (4096, 14336)]
+    announce(f"decode small batch M={m}, 8B layer, random data")
+    host, lins = [], []
+    for i, (n, k) in enumerate(shapes):
+        p, s = wl.random_words_host(300 + i, n, k), wl.random_scales_host(310 + i, n, k)
+        x = wl.x_host(320 + i + m, m, k)
+        host.append((p, s, x))
+        lins.append((to_dev(p), to_dev(s), to_dev(x), nan_out(m, n)))
+    run(lins, m=m)
+    for (p, s, x), lin, (n, k) in zip(host, lins, shapes):
+        rows = np.sort(np.random.default_rng(n + k).choice(n, size=min(n, 256), replace=False))
+        pr, sr = np.ascontiguousarray(p[rows]), np.ascontiguousarray(s[rows])
+        y = to_host(lin[3], np.float16)[:, rows]
+        ok = oracle.within_tolerance(y, oracle.gemv(pr, sr, x, len(rows), k), oracle.tol_bound(pr, sr, x, len(rows), k))
+        assert ok.all(), f"M={m} {n}x{k}: {(~ok).sum()} outside tolerance"
