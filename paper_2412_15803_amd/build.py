@@ -41,14 +41,18 @@ COMPILE_FLAGS = [
 ]
 
 
-def source_hash() -> str:
-    """Short hash of the HIP sources the kernels are built from (csrc/);
-    profile summaries record it so that figures taken from an older kernel
-    are recognised as stale."""
+# Sources the batch-1 decode-step kernel and its launch plan are built from.
+STEP_KERNEL_SOURCES = ("wq_api.hip", "wq_decode.hip", "wq_device.h", "wq_internal.h")
+
+
+def source_hash(names=STEP_KERNEL_SOURCES) -> str:
+    """Short hash of the named HIP sources under csrc/; profile summaries
+    record it so that figures taken from an older kernel are recognised as
+    stale."""
     import hashlib
 
     h = hashlib.sha256()
-    files = sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.h")))
+    files = sorted(os.path.join(CSRC, n) for n in names)
     for f in files:
         h.update(os.path.basename(f).encode())
         with open(f, "rb") as fh:
