@@ -503,7 +503,7 @@ wq_status wq_decode_linears(const wq_linear* linears, int64_t count, int64_t M, 
     (void)hipGetLastError();
     const hipStream_t s = static_cast<hipStream_t>(stream);
     if (M == 1) return decode_grouped(fn, lin, s);
-    if (M <= 64) return decode_grouped_batch(fn, lin, M, s);
+    if (M >= wq::kMatrixCoreMinM && M <= 64 && !wq::vector_small_batch()) return decode_grouped_batch(fn, lin, M, s);
     // Larger batches: one launch per linear, in stream order.
     return decode_per_linear(fn, lin.data(), count, M, s);
 }

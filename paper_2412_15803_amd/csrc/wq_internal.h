@@ -16,6 +16,14 @@ hipError_t launch_gemv(const uint32_t* packed, const uint16_t* scales,
                        const uint16_t* x, uint16_t* y,
                        int64_t n, int64_t k, int64_t m, hipStream_t stream);
 
+// Smallest batch that uses the matrix cores; smaller batches run on the
+// vector ALUs.
+constexpr int kMatrixCoreMinM = 8;
+
+// WQ_SMALL_BATCH_VECTOR=1 in the environment sends every small batch to the
+// vector kernel (for comparing the two paths; read at every call).
+bool vector_small_batch();
+
 // y[M][N] for 2 <= M on the matrix cores, 16 batch rows per launch.
 hipError_t launch_gemm_mfma(const uint32_t* packed, const uint16_t* scales, const uint16_t* x, uint16_t* y,
                             int64_t n, int64_t k, int64_t m, hipStream_t stream);

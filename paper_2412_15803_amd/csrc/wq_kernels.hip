@@ -2,6 +2,8 @@
 #include "wq_device.h"
 #include "wq_internal.h"
 
+#include <cstdlib>
+
 namespace wq {
 namespace {
 
@@ -9,6 +11,7 @@ using namespace dev;
 
 constexpr int kBlock = 256;  // 4 waves per workgroup
 constexpr int kWavesPerBlock = kBlock / kWave;
+constexpr int kTargetWaves = 256 * 8;  // 256 CUs x 8 waves
 
 // --------------------------------------------------------------- quantize
 //
@@ -106,6 +109,125 @@ __global__ __launch_bounds__(kBlock) void gemv_m1_kernel(const u32x4* packed, co
     flush_y(y, rb, ylds, (int)(re - rb), lane);
 }
 
+// ------------------------------------------------ small batches, vector ALUs
+//
+// For 2 <= M <= 8 batch rows per pass.  A wave owns rows [rb, re) (at most
+// kMbRows) and walks the row's groups in tiles of 64: lane l takes group
+// 64 kt + l of every row.  Per tile it loads x of its group for the MB batch
+// rows into registers (pre-paired like the batch-1 kernels), then streams
+// its rows kMbU at a time through two register buffers (buffer-resource
+// loads, as in the batch-1 kernels).  Each row's MB dot products are reduced
+// across the wave with DPP, and lane 63 adds them to fp32 partial sums in
+// LDS; after the last tile the partials are rounded once to fp16.
+constexpr int kMbRows = 256;
+constexpr int kMbU = 4;
+
+template <int MB>
+struct MbBuf {
+    u32x4 w[kMbU];
+    uint32_t s[kMbU];
+};
+
+template <int MB>
+__device__ __forceinline__ void mb_issue(MbBuf<MB>& b, const LinearRsrc& r, int64_t row0, int kt, int ng,
+                                         int lane) {
+#pragma unroll
+    for (int u = 0; u < kMbU; ++u) {
+        const uint32_t go = (uint32_t)((row0 + u) * ng + 64 * kt);
+        b.w[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r.w, lane * 16, go * 16, 0));
+        b.s[u] = __builtin_amdgcn_raw_buffer_load_b16(r.s, lane * 2, go * 2, 0);
+    }
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+template <int MB>
+__device__ __forceinline__ void mb_compute(const MbBuf<MB>& b, const half2v (&xr)[MB][16], float* part,
+                                           int rel, int nrows, int lane) {
+#pragma unroll
+    for (int u = 0; u < kMbU; ++u) {
+        float acc[MB];
+#pragma unroll
+        for (int i = 0; i < MB; ++i) acc[i] = 0.0f;
+        const uint32_t wd[4] = {b.w[u].x, b.w[u].y, b.w[u].z, b.w[u].w};
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            half2v q[4];
+            dequant_word(wd[c], q);
+#pragma unroll
+            for (int i = 0; i < MB; ++i)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) acc[i] = __builtin_amdgcn_fdot2(q[e], xr[i][4 * c + e], acc[i], false);
+        }
+        const float sc = __half2float(__ushort_as_half((uint16_t)b.s[u]));
+#pragma unroll
+        for (int i = 0; i < MB; ++i) {
+            const float tot = segment_sum<kWave>(sc * acc[i]);
+            if (lane == kWave - 1 && u < nrows) part[(rel + u) * MB + i] += tot;
+        }
+    }
+}
+
+template <int MB>
+__global__ __launch_bounds__(kBlock) void gemv_mb_kernel(const void* packed, const uint16_t* scales,
+                                                         const uint16_t* __restrict__ x, uint16_t* __restrict__ y,
+                                                         int64_t n, int ng, int m, int64_t rows_per_wave) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t wave = (int64_t)__builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerBlock + threadIdx.x / kWave);
+    const int64_t rb = wave * rows_per_wave;
+    if (rb >= n) return;
+    const int64_t re = min(n, rb + rows_per_wave);
+    const int nrow = (int)(re - rb);
+    const int64_t steps = (nrow + kMbU - 1) / kMbU;
+    const LinearRsrc rs = make_rsrc(packed, scales, (uint32_t)(n * ng * 2));
+    const int64_t k = (int64_t)ng * kGroup;
+
+    __shared__ float s_part[kWavesPerBlock][kMbRows * MB];
+    float* part = s_part[threadIdx.x / kWave];
+    for (int i = lane; i < nrow * MB; i += kWave) part[i] = 0.0f;
+    wave_lds_sync();
+
+    const int ntiles = (ng + 63) / 64;
+    for (int kt = 0; kt < ntiles; ++kt) {
+        const int g = 64 * kt + lane;
+        const bool act = g < ng;
+        half2v xr[MB][16];
+#pragma unroll
+        for (int i = 0; i < MB; ++i) {
+            const int mi = min(i, m - 1);  // rows past m repeat the last one (never stored)
+            load_x_group(x + mi * k + (int64_t)min(g, ng - 1) * kGroup, xr[i]);
+#pragma unroll
+            for (int e = 0; e < 16; ++e) xr[i][e] = act ? xr[i][e] : half2v{(_Float16)0.0f, (_Float16)0.0f};
+        }
+        MbBuf<MB> a, b;
+        for (int64_t s = -2; s < steps; s += 2) {
+            if (s >= 0) mb_compute<MB>(a, xr, part, (int)(s * kMbU), nrow - (int)(s * kMbU), lane);
+            mb_issue<MB>(a, rs, rb + (s + 2) * kMbU, kt, ng, lane);
+            if (s + 1 >= 0 && s + 1 < steps)
+                mb_compute<MB>(b, xr, part, (int)((s + 1) * kMbU), nrow - (int)((s + 1) * kMbU), lane);
+            mb_issue<MB>(b, rs, rb + (s + 3) * kMbU, kt, ng, lane);
+        }
+    }
+    wave_lds_sync();
+    for (int i = lane; i < nrow * MB; i += kWave) {
+        const int r = i / MB, mi = i % MB;
+        if (mi < m) gbl(y)[mi * n + rb + r] = __half_as_ushort(__float2half_rn(part[i]));
+    }
+}
+
+template <int MB>
+hipError_t launch_mb(const uint32_t* packed, const uint16_t* scales, const uint16_t* x, uint16_t* y, int64_t n,
+                     int64_t ng, int m, hipStream_t stream) {
+    const int64_t steps = (n + kMbU - 1) / kMbU;
+    const int64_t spw = min((steps + kTargetWaves - 1) / kTargetWaves, (int64_t)(kMbRows / kMbU));
+    const int64_t rows_per_wave = spw * kMbU;
+    const int64_t waves = (n + rows_per_wave - 1) / rows_per_wave;
+    const int64_t blocks = (waves + kWavesPerBlock - 1) / kWavesPerBlock;
+    hipLaunchKernelGGL((gemv_mb_kernel<MB>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, packed, scales, x, y,
+                       n, (int)ng, m, rows_per_wave);
+    return hipGetLastError();
+}
+
 // ------------------------------------------------------- generic GEMV (any M)
 //
 // One wave per (row, chunk of up to MC batch rows), grid-stride; lanes stride
@@ -149,7 +271,6 @@ __global__ __launch_bounds__(kBlock) void gemv_generic_kernel(const u32x4* packe
     }
 }
 
-constexpr int kTargetWaves = 256 * 8;  // 256 CUs x 8 waves
 
 template <int LPR, int GPL>
 hipError_t launch_m1(const uint32_t* packed, const uint16_t* scales, const uint16_t* x, uint16_t* y,
@@ -168,6 +289,11 @@ hipError_t launch_m1(const uint32_t* packed, const uint16_t* scales, const uint1
 }
 
 }  // namespace
+
+bool vector_small_batch() {
+    const char* e = std::getenv("WQ_SMALL_BATCH_VECTOR");
+    return e && e[0] == '1';
+}
 
 hipError_t launch_pack(const float* w, uint32_t* packed, uint16_t* scales, int64_t n, int64_t k,
                        hipStream_t stream) {
@@ -191,7 +317,22 @@ hipError_t launch_gemv(const uint32_t* packed, const uint16_t* scales, const uin
         WQ_M1_CASE(16, 1) WQ_M1_CASE(16, 3) WQ_M1_CASE(16, 5) WQ_M1_CASE(16, 7)
 #undef WQ_M1_CASE
     }
-    if (m >= 2 && m <= 64 && fits_rsrc(n, ng)) return launch_gemm_mfma(packed, scales, x, y, n, k, m, stream);
+    if (m >= 2 && m <= 64 && fits_rsrc(n, ng)) {
+        // Matrix cores from 8 batch rows on (measured faster than the vector
+        // kernel there); below that, or when asked to, the vector kernel in
+        // passes of up to 8 rows.
+        if (m >= kMatrixCoreMinM && !vector_small_batch()) return launch_gemm_mfma(packed, scales, x, y, n, k, m, stream);
+        for (int64_t m0 = 0; m0 < m; m0 += 8) {
+            const int mc = (int)min((int64_t)8, m - m0);
+            const uint16_t* xc = x + m0 * k;
+            uint16_t* yc = y + m0 * n;
+            const hipError_t e = mc <= 2   ? launch_mb<2>(packed, scales, xc, yc, n, ng, mc, stream)
+                                 : mc <= 4 ? launch_mb<4>(packed, scales, xc, yc, n, ng, mc, stream)
+                                           : launch_mb<8>(packed, scales, xc, yc, n, ng, mc, stream);
+            if (e != hipSuccess) return e;
+        }
+        return hipSuccess;
+    }
     constexpr int MC = 4;
     const int64_t mchunks = (m + MC - 1) / MC;
     const int64_t waves = n * mchunks;
