@@ -249,9 +249,9 @@ def per_config(device, seed):
     res["unit"] = "[us per call, GB/s]"
     steps3 = [(lin.n, lin.k) for lin in wl.LLAMA3B_LAYER] * 28 + [(wl.LLAMA3B_LM_HEAD.n, wl.LLAMA3B_LM_HEAD.k)]
     steps8 = [(lin.n, lin.k) for lin in wl.LLAMA8B_LAYER] * 32 + [(128256, 4096)]
-    for m, v in time_step_batches(steps3, [4, 16], gen, device, 20, 3).items():
+    for m, v in time_step_batches(steps3, [4, 8, 16], gen, device, 20, 3).items():
         res[f"3B step M={m} (one wq_decode_linears call, 113 linears)"] = v
-    for m, v in time_step_batches(steps8, [1, 4, 16], gen, device, 20, 3).items():
+    for m, v in time_step_batches(steps8, [1, 4, 8, 16], gen, device, 20, 3).items():
         res[f"8B step M={m} (one wq_decode_linears call, 129 linears)"] = v
     return res
 

@@ -391,7 +391,41 @@ BatchPlan plan_batch_group(const std::vector<wq_linear>& lin, const Group& g, st
     return bp;
 }
 
-// M >= 2: one matrix-core launch per dependency group and 16 batch rows.
+// 2 <= M < 8 on the vector ALUs: one launch per dependency group and 8
+// batch rows; waves own fixed-size row runs of one linear each.
+BatchPlan plan_vector_group(const std::vector<wq_linear>& lin, const Group& g, std::vector<unsigned char>& bytes) {
+    const int count = g.end - g.begin;
+    int64_t total_rows = 0;
+    for (int i = 0; i < count; ++i) total_rows += lin[g.begin + i].N;
+    const int rows = wq::mb_rows_per_wave(total_rows);
+    std::vector<wq::DecodeEntry> ents(count, wq::DecodeEntry{});
+    int64_t waves = 0;
+    for (int i = 0; i < count; ++i) {
+        const wq_linear& l = lin[g.begin + i];
+        wq::DecodeEntry& e = ents[i];
+        e.packed = l.packed_w;
+        e.scales = l.scales;
+        e.x = l.x;
+        e.y = l.y;
+        e.n = l.N;
+        e.ng = (int32_t)(l.K / 32);
+        e.pad = rows;
+        e.first_step = waves;
+        e.steps = (l.N + rows - 1) / rows;
+        waves += e.steps;
+    }
+    BatchPlan bp;
+    bp.count = count;
+    bp.blocks = waves;  // waves, for this plan
+    bp.waves_per_block = 0;
+    bp.off_entries = align16(bytes.size());
+    bytes.resize(align16(bp.off_entries + sizeof(wq::DecodeEntry) * count), 0);
+    std::memcpy(bytes.data() + bp.off_entries, ents.data(), sizeof(wq::DecodeEntry) * count);
+    return bp;
+}
+
+// M >= 2: one matrix-core launch per dependency group and 16 batch rows
+// (from kMatrixCoreMinM rows on), else one vector launch per group and 8.
 wq_status decode_grouped_batch(const char* fn, const std::vector<wq_linear>& lin, int64_t m, hipStream_t stream) {
     const std::vector<Group> groups = split_groups(lin, m);
     std::lock_guard<std::mutex> guard(g_ws_mu);
@@ -399,9 +433,11 @@ wq_status decode_grouped_batch(const char* fn, const std::vector<wq_linear>& lin
     wq_status st = get_workspace(fn, stream, ws);
     if (st != WQ_OK) return st;
     std::vector<unsigned char> bytes;
+    const bool matrix = m >= wq::kMatrixCoreMinM && !wq::vector_small_batch();
     std::vector<BatchPlan> plans(groups.size());
     for (size_t i = 0; i < groups.size(); ++i)
-        if (groups[i].grouped) plans[i] = plan_batch_group(lin, groups[i], bytes);
+        if (groups[i].grouped)
+            plans[i] = matrix ? plan_batch_group(lin, groups[i], bytes) : plan_vector_group(lin, groups[i], bytes);
     if (!bytes.empty() && (st = upload_plan(fn, ws, bytes, stream)) != WQ_OK) return st;
     for (size_t i = 0; i < groups.size(); ++i) {
         const Group& g = groups[i];
@@ -411,9 +447,11 @@ wq_status decode_grouped_batch(const char* fn, const std::vector<wq_linear>& lin
         }
         const BatchPlan& bp = plans[i];
         const wq::DecodeEntry* ents = reinterpret_cast<const wq::DecodeEntry*>(ws->d_plan + bp.off_entries);
-        for (int64_t m0 = 0; m0 < m; m0 += 16) {
-            const int mc = (int)std::min<int64_t>(16, m - m0);
-            st = hip_status(fn, wq::launch_grouped_mfma(ents, bp.count, bp.blocks, bp.waves_per_block, m0, mc, stream));
+        const int64_t chunk = matrix ? 16 : 8;
+        for (int64_t m0 = 0; m0 < m; m0 += chunk) {
+            const int mc = (int)std::min<int64_t>(chunk, m - m0);
+            st = hip_status(fn, matrix ? wq::launch_grouped_mfma(ents, bp.count, bp.blocks, bp.waves_per_block, m0, mc, stream)
+                                       : wq::launch_grouped_mb(ents, bp.count, bp.blocks, m0, mc, stream));
             if (st != WQ_OK) return st;
         }
     }
@@ -503,7 +541,7 @@ wq_status wq_decode_linears(const wq_linear* linears, int64_t count, int64_t M, 
     (void)hipGetLastError();
     const hipStream_t s = static_cast<hipStream_t>(stream);
     if (M == 1) return decode_grouped(fn, lin, s);
-    if (M >= wq::kMatrixCoreMinM && M <= 64 && !wq::vector_small_batch()) return decode_grouped_batch(fn, lin, M, s);
+    if (M <= 64) return decode_grouped_batch(fn, lin, M, s);
     // Larger batches: one launch per linear, in stream order.
     return decode_per_linear(fn, lin.data(), count, M, s);
 }

@@ -41,7 +41,7 @@ struct DecodeEntry {
     int32_t ng;              // groups of 32 per row
     int32_t lpr;             // lanes per row (16, 32 or 64)
     int32_t gpl;             // groups per lane (lpr * gpl >= ng)
-    int32_t pad;
+    int32_t pad;             // rows per wave (small-batch vector launches)
 };
 static_assert(sizeof(DecodeEntry) == 72, "DecodeEntry layout");
 
@@ -74,6 +74,14 @@ struct DecodePlan {
 int grouped_mfma_tiles();
 hipError_t launch_grouped_mfma(const DecodeEntry* entries, int count, int64_t blocks, int waves_per_block,
                                int64_t m0, int m, hipStream_t stream);
+
+// Small-batch decode step below kMatrixCoreMinM rows: independent linears in
+// one launch of the vector kernel.  Entry i owns waves [first_step,
+// first_step + steps) of the grid, `pad` rows each (mb_rows_per_wave of the
+// launch's total rows); batch rows [m0, m0 + m), m <= 8.
+hipError_t launch_grouped_mb(const DecodeEntry* entries, int count, int64_t waves, int64_t m0, int m,
+                             hipStream_t stream);
+int mb_rows_per_wave(int64_t total_rows);
 
 // Largest groups-per-lane of the grouped kernel (K <= 16384).
 constexpr int kDecodeMaxGpl = 8;

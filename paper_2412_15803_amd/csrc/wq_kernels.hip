@@ -168,22 +168,14 @@ __device__ __forceinline__ void mb_compute(const MbBuf<MB>& b, const half2v (&xr
     }
 }
 
+// Rows [rb, re) of one linear (re - rb <= kMbRows), batch rows [0, m).
 template <int MB>
-__global__ __launch_bounds__(kBlock) void gemv_mb_kernel(const void* packed, const uint16_t* scales,
-                                                         const uint16_t* __restrict__ x, uint16_t* __restrict__ y,
-                                                         int64_t n, int ng, int m, int64_t rows_per_wave) {
-    const int lane = threadIdx.x & (kWave - 1);
-    const int64_t wave = (int64_t)__builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerBlock + threadIdx.x / kWave);
-    const int64_t rb = wave * rows_per_wave;
-    if (rb >= n) return;
-    const int64_t re = min(n, rb + rows_per_wave);
+__device__ __forceinline__ void mb_range(const void* packed, const uint16_t* scales, const uint16_t* x, uint16_t* y,
+                                         int64_t n, int ng, int m, int64_t rb, int64_t re, float* part, int lane) {
     const int nrow = (int)(re - rb);
     const int64_t steps = (nrow + kMbU - 1) / kMbU;
     const LinearRsrc rs = make_rsrc(packed, scales, (uint32_t)(n * ng * 2));
     const int64_t k = (int64_t)ng * kGroup;
-
-    __shared__ float s_part[kWavesPerBlock][kMbRows * MB];
-    float* part = s_part[threadIdx.x / kWave];
     for (int i = lane; i < nrow * MB; i += kWave) part[i] = 0.0f;
     wave_lds_sync();
 
@@ -213,6 +205,42 @@ __global__ __launch_bounds__(kBlock) void gemv_mb_kernel(const void* packed, con
         const int r = i / MB, mi = i % MB;
         if (mi < m) gbl(y)[mi * n + rb + r] = __half_as_ushort(__float2half_rn(part[i]));
     }
+    wave_lds_sync();  // the slice is free again
+}
+
+template <int MB>
+__global__ __launch_bounds__(kBlock) void gemv_mb_kernel(const void* packed, const uint16_t* scales,
+                                                         const uint16_t* __restrict__ x, uint16_t* __restrict__ y,
+                                                         int64_t n, int ng, int m, int64_t rows_per_wave) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t wave = (int64_t)__builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerBlock + threadIdx.x / kWave);
+    const int64_t rb = wave * rows_per_wave;
+    if (rb >= n) return;
+    __shared__ float s_part[kWavesPerBlock][kMbRows * MB];
+    mb_range<MB>(packed, scales, x, y, n, ng, m, rb, min(n, rb + rows_per_wave), s_part[threadIdx.x / kWave], lane);
+}
+
+// Independent linears of a decode step in one launch: entry i owns waves
+// [first_step, first_step + steps), each `pad` rows of it (found by binary
+// search over the entries); batch rows [m0, m0 + m).
+template <int MB>
+__global__ __launch_bounds__(kBlock) void grouped_mb_kernel(const DecodeEntry* __restrict__ entries, int count,
+                                                            int64_t waves, int64_t m0, int m) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t wave = (int64_t)__builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerBlock + threadIdx.x / kWave);
+    if (wave >= waves) return;
+    int lo = 0, hi = count - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) / 2;
+        if (entries[mid].first_step <= wave) lo = mid;
+        else hi = mid - 1;
+    }
+    const DecodeEntry& e = entries[lo];
+    const int64_t rb = (wave - e.first_step) * e.pad;
+    const int64_t k = (int64_t)e.ng * kGroup;
+    __shared__ float s_part[kWavesPerBlock][kMbRows * MB];
+    mb_range<MB>(e.packed, e.scales, e.x + m0 * k, e.y + m0 * e.n, e.n, e.ng, m, rb, min(e.n, rb + e.pad),
+                 s_part[threadIdx.x / kWave], lane);
 }
 
 template <int MB>
@@ -289,6 +317,27 @@ hipError_t launch_m1(const uint32_t* packed, const uint16_t* scales, const uint1
 }
 
 }  // namespace
+
+hipError_t launch_grouped_mb(const DecodeEntry* entries, int count, int64_t waves, int64_t m0, int m,
+                             hipStream_t stream) {
+    const int64_t blocks = (waves + kWavesPerBlock - 1) / kWavesPerBlock;
+    if (m <= 2)
+        hipLaunchKernelGGL((grouped_mb_kernel<2>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, entries, count,
+                           waves, m0, m);
+    else if (m <= 4)
+        hipLaunchKernelGGL((grouped_mb_kernel<4>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, entries, count,
+                           waves, m0, m);
+    else
+        hipLaunchKernelGGL((grouped_mb_kernel<8>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, entries, count,
+                           waves, m0, m);
+    return hipGetLastError();
+}
+
+int mb_rows_per_wave(int64_t total_rows) {
+    // About 2048 waves over the whole launch, at most kMbRows rows each.
+    const int64_t r = (total_rows + kTargetWaves - 1) / kTargetWaves;
+    return (int)min((int64_t)kMbRows, max((int64_t)kMbU, (r + kMbU - 1) / kMbU * kMbU));
+}
 
 bool vector_small_batch() {
     const char* e = std::getenv("WQ_SMALL_BATCH_VECTOR");
