@@ -1,6 +1,8 @@
 // Small-batch 4-bit GEMM on the matrix cores: y[M][N] = x[M][K] dequant(W)^T
-// for 2 <= M <= 16 per launch (the concurrent-sequences decode of the
-// paper's serving engine, Sec. 2.2; GEMM tiling, Sec. 2.3).
+// for up to 16 batch rows per launch, used from M = 8 on (smaller batches
+// run on the vector kernel).  Batching several sequences is this library's
+// extension of the paper's batch-1 decoding; the tiling follows the
+// operator-level GEMM tiling the paper's compiler applies (Sec. 2.3).
 //
 // One v_mfma_f32_16x16x32_f16 multiplies a 16 x 32 block of x (16 batch
 // rows, one 32-element group) by the dequantized 32 x 16 block of W^T (the
