@@ -326,3 +326,35 @@ def test_small_batch_decode_random_data_tolerance(m):
         y = to_host(lin[3], np.float16)[:, rows]
         ok = oracle.within_tolerance(y, oracle.gemv(pr, sr, x, len(rows), k), oracle.tol_bound(pr, sr, x, len(rows), k))
         assert ok.all(), f"M={m} {n}x{k}: {(~ok).sum()} outside tolerance"
+
+
+@pytest.mark.parametrize("m", [8, 16])
+def test_small_batch_both_paths_bit_exact(m, monkeypatch):
+    """From M = 8 on the matrix cores are the default; the vector kernel
+    (forced through WQ_SMALL_BATCH_VECTOR, read by the library at every call)
+    must give the same exact results, single GEMV and decode step alike."""
+    from paper_2412_15803_amd import wq
+
+    rng = np.random.default_rng(400 + m)
+    shapes = [(4096, 4096), (1000, 14336), (257, 2080)]
+    host, data = [], []
+    for n, k in shapes:
+        p, s = int_linear(rng, n, k, 1 / 8)
+        x = rng.integers(-1, 2, size=(m, k)).astype(np.float16)
+        host.append((p, s, x))
+        data.append((to_dev(p), to_dev(s), to_dev(x)))
+    for vector in (False, True):
+        if vector:
+            monkeypatch.setenv("WQ_SMALL_BATCH_VECTOR", "1")
+        else:
+            monkeypatch.delenv("WQ_SMALL_BATCH_VECTOR", raising=False)
+        announce(f"small batch M={m} {'vector' if vector else 'matrix-core'} path")
+        lins = [(p, s, x, nan_out(m, n)) for (p, s, x), (n, k) in zip(data, shapes)]
+        run(lins, m=m)
+        for (p, s, x), lin, (n, k) in zip(host, lins, shapes):
+            ref = oracle.gemv(p, s, x, n, k)
+            check_exact(lin[3], ref, f"decode M={m} {n}x{k} vector={vector}")
+            y1 = nan_out(m, n)
+            wq.wq_gemv(lin[0], lin[1], lin[2], y1)
+            check_exact(y1, ref, f"gemv M={m} {n}x{k} vector={vector}")
+    monkeypatch.delenv("WQ_SMALL_BATCH_VECTOR", raising=False)
