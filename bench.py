@@ -228,6 +228,31 @@ def time_step_batches(shapes, batches, gen, device, steps, warmup):
     return out
 
 
+def time_pack(n, k, gen, device, calls=10):
+    """wq_pack of an fp32 W[n][k] already on the device: us per call and GB/s
+    of its bytes (4 read + 0.5625 written per weight)."""
+    import torch
+
+    from paper_2412_15803_amd import wq
+
+    w = torch.randn((n, k), device=device, generator=gen).mul_(0.02)
+    packed = torch.empty((n, k // 8), dtype=torch.int32, device=device)
+    scales = torch.empty((n, k // 32), dtype=torch.float16, device=device)
+    wq.wq_pack(w, packed, scales)
+    torch.cuda.synchronize()
+    a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(calls):
+        wq.wq_pack(w, packed, scales)
+    e.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(e) / calls
+    nbytes = n * k * 4 + n * k // 2 + n * (k // 32) * 2
+    del w, packed, scales
+    torch.cuda.empty_cache()
+    return [round(ms * 1e3, 2), round(nbytes / (ms * 1e-3) / 1e9, 1)]
+
+
 def per_config(device, seed):
     """Per-shape figures beside the headline step (SURVEY configs 1-4 and the
     8B-class step); none of them is the bench value."""
@@ -240,6 +265,7 @@ def per_config(device, seed):
     res = {"method": "single wq_gemv calls rotated over >= 1 GiB of weight copies, replayed from a HIP graph "
                      "(device time per call, host launch excluded); random codes and scales of each shape"}
     res["512x512 M=1"] = time_gemv_rotated(512, 512, [1], gen, device)[1]
+    res["wq_pack 8B gate_up 28672x4096 (fp32 in, codes + scales out)"] = time_pack(28672, 4096, gen, device)
     for lin in wl.LLAMA3B_LAYER + (wl.LLAMA3B_LM_HEAD,):
         res[f"3B {lin.name} {lin.n}x{lin.k} M=1"] = time_gemv_rotated(lin.n, lin.k, [1], gen, device)[1]
     for lin in wl.LLAMA8B_LAYER:

@@ -70,6 +70,21 @@ def decode_step_linears(base_seed: int = 1234):
     return out
 
 
+def decode_step_linears_8b(base_seed: int = 4321):
+    """The 8B-class step: 32 x (qkv, o, gate_up, down) + lm_head 128256x4096.
+
+    Returns a list of (Linear, weight_seed, x_seed) in execution order.
+    """
+    out = []
+    for layer in range(32):
+        for lid, lin in enumerate(LLAMA8B_LAYER):
+            ws = base_seed + 10 * layer + lid
+            out.append((Linear(f"l{layer}.{lin.name}", lin.n, lin.k), ws, ws + 100_000))
+    ws = base_seed + 999
+    out.append((Linear("lm_head", 128256, 4096), ws, ws + 100_000))
+    return out
+
+
 def ideal_bytes(n: int, k: int, m: int) -> int:
     """Bytes a decode linear must move at least once: packed 4-bit codes,
     fp16 group scales, fp16 x and fp16 y."""

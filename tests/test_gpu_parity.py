@@ -371,3 +371,38 @@ def test_decode_step_3b_sampled():
         yg = to_host(y, np.float16)[:, rows]
         ok = oracle.within_tolerance(yg, y_ref, oracle.tol_bound(rp, rs, xh, len(rows), lin.k))
         assert ok.all(), lin.name
+
+
+@pytest.mark.parametrize("m", [1, 8])
+def test_decode_step_8b_sampled(m):
+    """The 8B-class decode step (32 layers + lm_head, 129 linears, K up to
+    14336) in one wq_decode_linears call at M = 1 (batch-1 grouped kernel)
+    and M = 8 (matrix-core grouped kernel), weights generated on the device
+    and packed by the library; every linear checked on sampled rows."""
+    import torch
+
+    from paper_2412_15803_amd import wq
+
+    plan = wl.decode_step_linears_8b()
+    announce(f"8B decode step M={m}: building {len(plan)} linears")
+    lins, checks = [], []
+    for idx, (lin, ws, xs) in enumerate(plan):
+        w = wl.weights_device(ws, lin.n, lin.k)
+        packed, scales = gpu_pack(w)
+        rows = sample_rows(lin.n, 16, 1000 + idx)
+        w_rows = w[torch.from_numpy(rows).to(w.device)].cpu().numpy()
+        del w
+        x = wl.x_device(xs, m, lin.k)
+        y = torch.full((m, lin.n), float("nan"), dtype=torch.float16, device="cuda")
+        lins.append((packed, scales, x, y))
+        checks.append((lin, rows, w_rows))
+    announce(f"8B decode step M={m}: running wq_decode_linears")
+    wq.wq_decode_linears(lins, m=m)
+    torch.cuda.synchronize()
+    for (packed, scales, x, y), (lin, rows, w_rows) in zip(lins, checks):
+        rp, rs = oracle.quantize_pack(w_rows)
+        xh = to_host(x, np.float16)
+        y_ref = oracle.gemv(rp, rs, xh, len(rows), lin.k)
+        y_gpu = to_host(y, np.float16)[:, rows]
+        ok = oracle.within_tolerance(y_gpu, y_ref, oracle.tol_bound(rp, rs, xh, len(rows), lin.k))
+        assert ok.all(), f"{lin.name}: {(~ok).sum()} outside tolerance"
