@@ -15,3 +15,12 @@ from .wq_oracle import (  # noqa: F401
     unpack,
     within_tolerance,
 )
+from .attn_oracle import (  # noqa: F401
+    ATTN_ABS_TOL,
+    ATTN_MAX_SCORE_BOUND,
+    ATTN_REL_TOL,
+    attn_tol_bound,
+    attn_within_tolerance,
+    decode_attention,
+    decode_attention_f64,
+)
