@@ -459,6 +459,8 @@ wq_status decode_grouped_batch(const char* fn, const std::vector<wq_linear>& lin
 }
 }  // namespace
 
+wq_status wq::record_error(wq_status st, const char* message) { return fail(st, "%s", message); }
+
 extern "C" {
 
 const char* wq_status_string(int status) {

@@ -1,0 +1,621 @@
+// Decode-step attention over a paged KV cache (gfx950, wave64): the attention
+// of one new token per sequence over the keys and values that the engine
+// keeps in a paged cache (Sec. 2.2), computed the way PagedAttention-style
+// kernels do (Sec. 2.3): scores, softmax and the weighted sum of values in
+// one pass over the cache, split along the sequence where one workgroup per
+// head would leave the chip idle.
+//
+// Work split.  A sequence is cut into chunks of T = 2^log2_chunk tokens.  One
+// 256-thread workgroup takes one (sequence, kv head, chunk) and serves all G
+// query heads of that kv head, so every cached key and value is read from HBM
+// once.  Each of its four waves takes a contiguous quarter of the chunk.
+//
+// Lane layout.  A wave-wide 16-byte load covers four tokens: lanes
+// 16r .. 16r + 15 (row r) hold dims 8c .. 8c + 7 (c = lane % 16) of token r,
+// 256 contiguous bytes per token.  A "block" is four such loads of keys and
+// four of values (16 tokens of one wave); blocks are double-buffered in
+// registers.  Scores are 16-lane DPP sums of v_dot2 partials (exact fp16
+// products, fp32 sums) and end up in every lane of the row.  Each row keeps a
+// running softmax state per query head: the maximum m of its scores (in
+// log2 units), l = sum 2^(a - m) and acc = sum 2^(a - m) V over its 8 dims,
+// rescaled once per block.
+//
+// Merging.  The four row states of a wave are merged across lanes, the four
+// wave states through LDS.  With one chunk per sequence the workgroup then
+// writes the fp16 output; otherwise it writes (m, l, acc) to the workspace
+// and merge_kernel combines the chunks of every (sequence, query head).
+#include <hip/hip_fp16.h>
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+
+#include "wq_attention.h"
+#include "wq_device.h"
+#include "wq_internal.h"
+
+namespace wq {
+namespace attn {
+namespace {
+
+using dev::as_h2;
+using dev::gbl;
+using dev::half2v;
+using dev::u32x4;
+
+constexpr int kD = WQ_ATTN_HEAD_DIM;
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
+constexpr int kRowsPerLoad = 4;                              // tokens per wave-wide load
+constexpr int kLoadsPerBlock = 4;
+constexpr int kBlockTokens = kRowsPerLoad * kLoadsPerBlock;  // 16 tokens of one wave
+constexpr int kMinLog2Chunk = 6;                             // 64 tokens: a block per wave
+constexpr int kMaxLog2Chunk = 12;
+constexpr int kMaxSplits = 1024;
+constexpr uint16_t kHalfNaN = 0x7E00;
+
+static_assert(kD == 128, "the lane layout assumes 16 lanes x 8 dims per token");
+static_assert((1 << kMinLog2Chunk) == kWaves * kBlockTokens, "a chunk holds whole blocks");
+
+struct Params {
+    const uint16_t* q;
+    const uint16_t* k;
+    const uint16_t* v;
+    const int32_t* table;
+    const int32_t* lens;
+    uint16_t* out;
+    float* part_acc;    // [seq * hq + h][splits][kD]
+    float2* part_ml;    // [seq * hq + h][splits]: (m, l)
+    int64_t max_pages;  // row length of the block table
+    uint32_t page_stride;  // elements per page: hkv * page_size * kD
+    int32_t num_pages;
+    int32_t hq, hkv;
+    int32_t log2_page;
+    int32_t log2_chunk;
+    int32_t splits;
+    int32_t max_seq_len;
+    int32_t pages_lds;  // bytes of LDS before the wave states
+    float c;            // scale * log2(e): scores in log2 units
+};
+
+__device__ __forceinline__ bool bad_length(const Params& p, int len) {
+    return len < 0 || len > p.max_seq_len || (int64_t)len > (p.max_pages << p.log2_page);
+}
+
+__device__ __forceinline__ uint16_t to_half_bits(float x) {
+    return __builtin_bit_cast(uint16_t, static_cast<_Float16>(x));
+}
+
+__device__ __forceinline__ float exp2_(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__device__ __forceinline__ float dot8(const half2v (&q)[4], const u32x4 k) {
+    float a = __builtin_amdgcn_fdot2(q[0], as_h2(k.x), 0.0f, false);
+    a = __builtin_amdgcn_fdot2(q[1], as_h2(k.y), a, false);
+    a = __builtin_amdgcn_fdot2(q[2], as_h2(k.z), a, false);
+    return __builtin_amdgcn_fdot2(q[3], as_h2(k.w), a, false);
+}
+
+__device__ __forceinline__ void unpack8(const u32x4 v, float (&f)[8]) {
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const half2v h = as_h2(w[i]);
+        f[2 * i] = static_cast<float>(h.x);
+        f[2 * i + 1] = static_cast<float>(h.y);
+    }
+}
+
+struct KVBlock {
+    u32x4 k[kLoadsPerBlock];
+    u32x4 v[kLoadsPerBlock];
+};
+
+// Running softmax state of one query head in one lane (8 dims of a row).
+struct State {
+    float m, l, acc[8];
+};
+
+// Merge the state of the lane `off` positions away (xor) into this one.
+__device__ __forceinline__ void merge_lanes(State& st, int off) {
+    const float m2 = __shfl_xor(st.m, off);
+    const float l2 = __shfl_xor(st.l, off);
+    const float mx = fmaxf(st.m, m2);
+    const float ms = mx == -INFINITY ? 0.0f : mx;
+    const float w1 = exp2_(st.m - ms), w2 = exp2_(m2 - ms);
+    st.l = st.l * w1 + l2 * w2;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const float a2 = __shfl_xor(st.acc[e], off);
+        st.acc[e] = st.acc[e] * w1 + a2 * w2;
+    }
+    st.m = mx;
+}
+
+template <int G>
+__global__ __launch_bounds__(kThreads) void split_kernel(const Params p) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    int* sh_pages = reinterpret_cast<int*>(smem);
+    float* sh_acc = reinterpret_cast<float*>(smem + p.pages_lds);  // [kWaves][G][kD]
+    float* sh_m = sh_acc + kWaves * G * kD;                           // [kWaves][G]
+    float* sh_l = sh_m + kWaves * G;
+
+    const int tid = threadIdx.x;
+    const int chunk = blockIdx.x % p.splits;
+    const int seq_kv = blockIdx.x / p.splits;
+    const int kvh = seq_kv % p.hkv;
+    const int s = seq_kv / p.hkv;
+    const int64_t head0 = (int64_t)s * p.hq + (int64_t)kvh * G;  // first query head of the group
+
+    const int len = p.lens[s];
+    if (bad_length(p, len) || len == 0) {
+        if (p.splits == 1) {
+            const uint16_t fill = len == 0 ? 0 : kHalfNaN;
+            for (int i = tid; i < G * kD; i += kThreads) p.out[head0 * kD + i] = fill;
+        }
+        return;
+    }
+    const int c0 = chunk << p.log2_chunk;
+    if (c0 >= len) return;
+
+    const int lane = tid & 63, row = lane >> 4, col = lane & 15;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+    // The query heads' 8 dims of this lane.
+    half2v qv[G][4];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+        const u32x4 t = *gbl(reinterpret_cast<const u32x4*>(p.q + (head0 + g) * kD + col * 8));
+        qv[g][0] = as_h2(t.x);
+        qv[g][1] = as_h2(t.y);
+        qv[g][2] = as_h2(t.z);
+        qv[g][3] = as_h2(t.w);
+    }
+
+    // Physical pages of the chunk's tokens, checked against the cache size.
+    const int log2_page = p.log2_page;
+    const int page_mask = (1 << log2_page) - 1;
+    const int first_page = c0 >> log2_page;
+    const int cend = min(c0 + (1 << p.log2_chunk), len);
+    const int npages = ((cend - 1) >> log2_page) - first_page + 1;
+    const int32_t* trow = p.table + (int64_t)s * p.max_pages + first_page;
+    int bad = 0;
+    for (int i = tid; i < npages; i += kThreads) {
+        int pg = trow[i];
+        if ((uint32_t)pg >= (uint32_t)p.num_pages) {
+            bad = 1;
+            pg = 0;
+        }
+        sh_pages[i] = pg;
+    }
+    const int any_bad = __syncthreads_or(bad);
+
+    // This wave's tokens: [wbase, wbase + wtok) intersected with [0, len).
+    const int wtok = 1 << (p.log2_chunk - 2);
+    const int wbase = c0 + wave * wtok;
+    const int nvalid = min(max(len - wbase, 0), wtok);
+    const int nblk = (nvalid + kBlockTokens - 1) / kBlockTokens;
+    const uint32_t head_slot0 = (uint32_t)kvh << log2_page;
+
+    // Loads of block `blk`.  Rows past the end of the sequence read its last
+    // token again (already cached) so that every block issues the same loads.
+    auto issue = [&](KVBlock& b, int blk) {
+#pragma unroll
+        for (int j = 0; j < kLoadsPerBlock; ++j) {
+            const int t = min(wbase + blk * kBlockTokens + j * kRowsPerLoad + row, len - 1);
+            const uint32_t pg = (uint32_t)sh_pages[(t >> log2_page) - first_page];
+            const uint64_t off = (uint64_t)pg * p.page_stride +
+                                 (uint64_t)((head_slot0 + (uint32_t)(t & page_mask)) * kD + col * 8);
+            b.k[j] = *gbl(reinterpret_cast<const u32x4*>(p.k + off));
+            b.v[j] = *gbl(reinterpret_cast<const u32x4*>(p.v + off));
+        }
+    };
+
+    State st[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+        st[g].m = -INFINITY;
+        st[g].l = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) st[g].acc[e] = 0.0f;
+    }
+
+    auto compute = [&](const KVBlock& b, int blk) {
+        float sc[G][kLoadsPerBlock];
+#pragma unroll
+        for (int j = 0; j < kLoadsPerBlock; ++j) {
+            const bool ok = wbase + blk * kBlockTokens + j * kRowsPerLoad + row < len;
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                const float d = dev::segment_sum<16>(dot8(qv[g], b.k[j]));
+                sc[g][j] = ok ? d * p.c : -INFINITY;
+            }
+        }
+        float vf[kLoadsPerBlock][8];
+#pragma unroll
+        for (int j = 0; j < kLoadsPerBlock; ++j) unpack8(b.v[j], vf[j]);
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            float mx = st[g].m;
+#pragma unroll
+            for (int j = 0; j < kLoadsPerBlock; ++j) mx = fmaxf(mx, sc[g][j]);
+            const float ms = mx == -INFINITY ? 0.0f : mx;
+            const float corr = exp2_(st[g].m - ms);
+            float l = st[g].l * corr;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) st[g].acc[e] *= corr;
+#pragma unroll
+            for (int j = 0; j < kLoadsPerBlock; ++j) {
+                const float pj = exp2_(sc[g][j] - ms);
+                l += pj;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) st[g].acc[e] = fmaf(pj, vf[j][e], st[g].acc[e]);
+            }
+            st[g].l = l;
+            st[g].m = mx;
+        }
+    };
+
+    // Double-buffered: the next block's loads are in flight while a block is
+    // computed.  Every path issues a buffer's loads before the other buffer's
+    // compute, so the compiler's wait counts stay exact.
+    if (nblk > 0) {
+        KVBlock a, b;
+        issue(a, 0);
+        int blk = 0;
+        bool last_in_a = true;
+        while (blk + 1 < nblk) {
+            issue(b, blk + 1);
+            compute(a, blk);
+            if (++blk + 1 >= nblk) {
+                last_in_a = false;
+                break;
+            }
+            issue(a, blk + 1);
+            compute(b, blk);
+            ++blk;
+        }
+        if (last_in_a) compute(a, blk);
+        else compute(b, blk);
+    }
+
+    // Merge the four rows of the wave, then the four waves.
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+        merge_lanes(st[g], 16);
+        merge_lanes(st[g], 32);
+    }
+    if (row == 0) {
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            float* dst = sh_acc + (wave * G + g) * kD + col * 8;
+            *reinterpret_cast<float4*>(dst) = make_float4(st[g].acc[0], st[g].acc[1], st[g].acc[2], st[g].acc[3]);
+            *reinterpret_cast<float4*>(dst + 4) = make_float4(st[g].acc[4], st[g].acc[5], st[g].acc[6], st[g].acc[7]);
+            if (col == 0) {
+                sh_m[wave * G + g] = st[g].m;
+                sh_l[wave * G + g] = st[g].l;
+            }
+        }
+    }
+    __syncthreads();
+    for (int i = tid; i < G * kD; i += kThreads) {
+        const int g = i / kD, d = i % kD;
+        float mx = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) mx = fmaxf(mx, sh_m[w * G + g]);
+        float l = 0.0f, acc = 0.0f;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) {
+            const float wt = exp2_(sh_m[w * G + g] - mx);
+            l = fmaf(sh_l[w * G + g], wt, l);
+            acc = fmaf(sh_acc[(w * G + g) * kD + d], wt, acc);
+        }
+        if (p.splits == 1) {
+            p.out[(head0 + g) * kD + d] = any_bad ? kHalfNaN : to_half_bits(acc / l);
+        } else {
+            const int64_t slot = (head0 + g) * p.splits + chunk;
+            p.part_acc[slot * kD + d] = acc;
+            if (d == 0) p.part_ml[slot] = make_float2(mx, any_bad ? NAN : l);
+        }
+    }
+}
+
+__device__ __forceinline__ float block_max(float v, float* sh) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+    if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
+    __syncthreads();
+    float r = sh[0];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) r = fmaxf(r, sh[w]);
+    return r;
+}
+
+__device__ __forceinline__ float block_sum(float v, float* sh) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
+    __syncthreads();
+    float r = sh[0];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) r += sh[w];
+    return r;
+}
+
+// One workgroup per (sequence, query head): out = sum_c 2^(m_c - M) acc_c /
+// sum_c 2^(m_c - M) l_c over the sequence's chunks, M = max_c m_c.
+__global__ __launch_bounds__(kThreads) void merge_kernel(const Params p) {
+    constexpr int kSlots = kThreads / (kD / 4);  // 8 chunk slots x 32 four-dim columns
+    __shared__ float sh_w[kMaxSplits];
+    __shared__ float sh_red[2][kWaves];
+    __shared__ float4 sh_part[kSlots][kD / 4];
+
+    const int tid = threadIdx.x;
+    const int64_t head = blockIdx.x;  // seq * hq + h
+    const int s = (int)(head / p.hq);
+    uint16_t* o = p.out + head * kD;
+    const int len = p.lens[s];
+    if (bad_length(p, len) || len == 0) {
+        if (tid < kD) o[tid] = len == 0 ? 0 : kHalfNaN;
+        return;
+    }
+    const int n = (len + (1 << p.log2_chunk) - 1) >> p.log2_chunk;
+    const float2* ml = p.part_ml + head * p.splits;
+    const float4* pa = reinterpret_cast<const float4*>(p.part_acc + head * p.splits * kD);
+
+    constexpr int kPer = kMaxSplits / kThreads;
+    float2 hdr[kPer];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < kPer; ++r) {
+        const int c = tid + r * kThreads;
+        hdr[r] = c < n ? ml[c] : make_float2(-INFINITY, 0.0f);
+        mx = fmaxf(mx, hdr[r].x);
+    }
+    mx = block_max(mx, sh_red[0]);
+    float l = 0.0f;
+#pragma unroll
+    for (int r = 0; r < kPer; ++r) {
+        const int c = tid + r * kThreads;
+        if (c < n) {
+            const float w = exp2_(hdr[r].x - mx);
+            sh_w[c] = w;
+            l = fmaf(hdr[r].y, w, l);
+        }
+    }
+    l = block_sum(l, sh_red[1]);  // its barrier also publishes sh_w
+
+    const int slot = tid / (kD / 4), dq = tid % (kD / 4);
+    float4 a = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    for (int c = slot; c < n; c += kSlots) {
+        const float w = sh_w[c];
+        const float4 v = pa[c * (kD / 4) + dq];
+        a.x = fmaf(w, v.x, a.x);
+        a.y = fmaf(w, v.y, a.y);
+        a.z = fmaf(w, v.z, a.z);
+        a.w = fmaf(w, v.w, a.w);
+    }
+    sh_part[slot][dq] = a;
+    __syncthreads();
+    if (tid < kD) {
+        const float* col = reinterpret_cast<const float*>(&sh_part[0][0]) + tid;
+        float acc = 0.0f;
+#pragma unroll
+        for (int sl = 0; sl < kSlots; ++sl) acc += col[sl * kD];
+        o[tid] = to_half_bits(acc / l);
+    }
+}
+
+// ------------------------------------------------------------------- host
+
+struct Plan {
+    int log2_chunk;
+    int64_t splits;
+    size_t ml_offset;  // bytes of part_acc
+    size_t ws_bytes;
+};
+
+int64_t target_blocks() {
+    const char* e = getenv("WQ_ATTN_TARGET_BLOCKS");
+    const long v = e ? strtol(e, nullptr, 10) : 0;
+    return v > 0 ? v : 1024;
+}
+
+// Chunk length: the smallest power of two from 64 tokens that keeps the
+// split launch within about target_blocks() workgroups and the chunks of a
+// sequence within kMaxSplits.
+Plan make_plan(int64_t seqs, int64_t hq, int64_t hkv, int64_t max_seq_len) {
+    const int64_t len = std::max<int64_t>(max_seq_len, 1);
+    auto splits_of = [&](int lc) { return (len + (int64_t(1) << lc) - 1) >> lc; };
+    const int64_t target = target_blocks();
+    int lc = kMinLog2Chunk;
+    while (lc < kMaxLog2Chunk && (splits_of(lc) > kMaxSplits || seqs * hkv * splits_of(lc) > target)) ++lc;
+    Plan pl{lc, splits_of(lc), 0, 0};
+    if (pl.splits > 1) {
+        pl.ml_offset = (size_t)(seqs * hq * pl.splits * kD * 4);
+        pl.ws_bytes = pl.ml_offset + (size_t)(seqs * hq * pl.splits * 8);
+    }
+    return pl;
+}
+
+template <int G>
+hipError_t launch_split(const Params& p, int64_t blocks, size_t lds, hipStream_t stream) {
+    hipLaunchKernelGGL(split_kernel<G>, dim3((unsigned)blocks), dim3(kThreads), lds, stream, p);
+    return hipGetLastError();
+}
+
+hipError_t launch(const Params& p, int group, int64_t seqs, hipStream_t stream) {
+    const int64_t blocks = seqs * p.hkv * p.splits;
+    const size_t lds = (size_t)p.pages_lds + (size_t)kWaves * group * (kD + 2) * 4;
+    hipError_t e;
+    switch (group) {
+        case 1: e = launch_split<1>(p, blocks, lds, stream); break;
+        case 2: e = launch_split<2>(p, blocks, lds, stream); break;
+        case 3: e = launch_split<3>(p, blocks, lds, stream); break;
+        case 4: e = launch_split<4>(p, blocks, lds, stream); break;
+        case 5: e = launch_split<5>(p, blocks, lds, stream); break;
+        case 6: e = launch_split<6>(p, blocks, lds, stream); break;
+        case 7: e = launch_split<7>(p, blocks, lds, stream); break;
+        default: e = launch_split<8>(p, blocks, lds, stream); break;
+    }
+    if (e != hipSuccess || p.splits == 1) return e;
+    hipLaunchKernelGGL(merge_kernel, dim3((unsigned)(seqs * p.hq)), dim3(kThreads), 0, stream, p);
+    return hipGetLastError();
+}
+
+wq_status err(wq_status st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+wq_status err(wq_status st, const char* fmt, ...) {
+    char msg[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(msg, sizeof(msg), fmt, ap);
+    va_end(ap);
+    return record_error(st, msg);
+}
+
+bool is_pow2(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
+int log2_of(int64_t v) {
+    int r = 0;
+    while ((int64_t(1) << r) < v) ++r;
+    return r;
+}
+bool aligned(const void* ptr, uintptr_t a) { return reinterpret_cast<uintptr_t>(ptr) % a == 0; }
+
+struct Span {
+    uintptr_t lo, hi;
+};
+Span span(const void* ptr, uint64_t bytes) {
+    const uintptr_t lo = reinterpret_cast<uintptr_t>(ptr);
+    return Span{lo, lo + (uintptr_t)bytes};
+}
+bool overlaps(Span a, Span b) { return a.lo < a.hi && b.lo < b.hi && a.lo < b.hi && b.lo < a.hi; }
+
+wq_status check_sizes(const char* fn, int64_t seqs, int64_t hq, int64_t hkv, int64_t head_dim,
+                      int64_t max_seq_len) {
+    if (seqs < 1 || seqs > WQ_ATTN_MAX_SEQS)
+        return err(WQ_ERR_INVALID_ARG, "%s: num_seqs must be in [1, %lld] (got %lld)", fn,
+                   (long long)WQ_ATTN_MAX_SEQS, (long long)seqs);
+    if (hkv < 1 || hkv > WQ_ATTN_MAX_KV_HEADS)
+        return err(WQ_ERR_INVALID_ARG, "%s: num_kv_heads must be in [1, %d] (got %lld)", fn,
+                   WQ_ATTN_MAX_KV_HEADS, (long long)hkv);
+    if (hq < 1 || hq % hkv != 0)
+        return err(WQ_ERR_INVALID_ARG, "%s: num_q_heads (%lld) must be a positive multiple of num_kv_heads (%lld)",
+                   fn, (long long)hq, (long long)hkv);
+    if (hq / hkv > WQ_ATTN_MAX_GROUP)
+        return err(WQ_ERR_UNSUPPORTED, "%s: at most %d query heads per kv head (got %lld)", fn,
+                   WQ_ATTN_MAX_GROUP, (long long)(hq / hkv));
+    if (head_dim != WQ_ATTN_HEAD_DIM)
+        return err(WQ_ERR_UNSUPPORTED, "%s: head_dim must be %d (got %lld)", fn, WQ_ATTN_HEAD_DIM,
+                   (long long)head_dim);
+    if (max_seq_len < 0 || max_seq_len > WQ_ATTN_MAX_SEQ_LEN)
+        return err(WQ_ERR_INVALID_ARG, "%s: max_seq_len must be in [0, %lld] (got %lld)", fn,
+                   (long long)WQ_ATTN_MAX_SEQ_LEN, (long long)max_seq_len);
+    const Plan pl = make_plan(seqs, hq, hkv, max_seq_len);
+    if (seqs * hkv * pl.splits > INT32_MAX || seqs * hq > INT32_MAX)
+        return err(WQ_ERR_INVALID_ARG, "%s: too many workgroups for one launch", fn);
+    return WQ_OK;
+}
+
+}  // namespace
+}  // namespace attn
+}  // namespace wq
+
+using namespace wq::attn;
+
+extern "C" {
+
+wq_status wq_paged_attention_workspace_size(int64_t num_seqs, int64_t num_q_heads, int64_t num_kv_heads,
+                                            int64_t head_dim, int64_t max_seq_len, size_t* bytes) {
+    static const char* fn = "wq_paged_attention_workspace_size";
+    if (!bytes) return err(WQ_ERR_INVALID_ARG, "%s: null output pointer", fn);
+    const wq_status st = check_sizes(fn, num_seqs, num_q_heads, num_kv_heads, head_dim, max_seq_len);
+    if (st != WQ_OK) return st;
+    *bytes = make_plan(num_seqs, num_q_heads, num_kv_heads, max_seq_len).ws_bytes;
+    return WQ_OK;
+}
+
+wq_status wq_paged_attention(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                             const int32_t* block_table, const int32_t* seq_lens, uint16_t* out,
+                             int64_t num_seqs, int64_t num_q_heads, int64_t num_kv_heads, int64_t head_dim,
+                             int64_t page_size, int64_t num_pages, int64_t max_pages_per_seq,
+                             int64_t max_seq_len, float scale, void* workspace, size_t workspace_bytes,
+                             void* stream) {
+    static const char* fn = "wq_paged_attention";
+    if (!q || !k_cache || !v_cache || !block_table || !seq_lens || !out)
+        return err(WQ_ERR_INVALID_ARG, "%s: null pointer", fn);
+    wq_status st = check_sizes(fn, num_seqs, num_q_heads, num_kv_heads, head_dim, max_seq_len);
+    if (st != WQ_OK) return st;
+    if (!is_pow2(page_size) || page_size > WQ_ATTN_MAX_PAGE_SIZE)
+        return err(WQ_ERR_UNSUPPORTED, "%s: page_size must be a power of two in [1, %d] (got %lld)", fn,
+                   WQ_ATTN_MAX_PAGE_SIZE, (long long)page_size);
+    if (num_pages < 1 || num_pages > INT32_MAX)
+        return err(WQ_ERR_INVALID_ARG, "%s: num_pages must be in [1, 2^31 - 1] (got %lld)", fn, (long long)num_pages);
+    if (max_pages_per_seq < 1 || max_pages_per_seq > INT32_MAX)
+        return err(WQ_ERR_INVALID_ARG, "%s: max_pages_per_seq must be in [1, 2^31 - 1] (got %lld)", fn,
+                   (long long)max_pages_per_seq);
+    if (max_seq_len > max_pages_per_seq * page_size)
+        return err(WQ_ERR_INVALID_ARG, "%s: max_seq_len %lld exceeds max_pages_per_seq * page_size", fn,
+                   (long long)max_seq_len);
+    if (!std::isfinite(scale)) return err(WQ_ERR_INVALID_ARG, "%s: scale must be finite", fn);
+    if (!aligned(q, 16) || !aligned(out, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16))
+        return err(WQ_ERR_MISALIGNED, "%s: q, out, k_cache and v_cache must be 16-byte aligned", fn);
+    if (!aligned(block_table, 4) || !aligned(seq_lens, 4))
+        return err(WQ_ERR_MISALIGNED, "%s: block_table and seq_lens must be 4-byte aligned", fn);
+
+    const Plan pl = make_plan(num_seqs, num_q_heads, num_kv_heads, max_seq_len);
+    if (pl.ws_bytes > 0) {
+        if (!workspace) return err(WQ_ERR_INVALID_ARG, "%s: a workspace of %zu bytes is needed", fn, pl.ws_bytes);
+        if (workspace_bytes < pl.ws_bytes)
+            return err(WQ_ERR_INVALID_ARG, "%s: workspace of %zu bytes is below the %zu needed", fn, workspace_bytes,
+                       pl.ws_bytes);
+        if (!aligned(workspace, 16)) return err(WQ_ERR_MISALIGNED, "%s: workspace must be 16-byte aligned", fn);
+    }
+    const uint64_t qo_bytes = (uint64_t)num_seqs * num_q_heads * head_dim * 2;
+    const uint64_t cache_bytes = (uint64_t)num_pages * num_kv_heads * page_size * head_dim * 2;
+    const Span so = span(out, qo_bytes);
+    const Span sw = span(workspace, pl.ws_bytes);
+    const Span inputs[] = {span(q, qo_bytes), span(k_cache, cache_bytes), span(v_cache, cache_bytes),
+                           span(block_table, (uint64_t)num_seqs * max_pages_per_seq * 4),
+                           span(seq_lens, (uint64_t)num_seqs * 4)};
+    for (const Span& in : inputs) {
+        if (overlaps(so, in)) return err(WQ_ERR_INVALID_ARG, "%s: out overlaps an input", fn);
+        if (overlaps(sw, in)) return err(WQ_ERR_INVALID_ARG, "%s: the workspace overlaps an input", fn);
+    }
+    if (overlaps(so, sw)) return err(WQ_ERR_INVALID_ARG, "%s: out overlaps the workspace", fn);
+
+    const int group = (int)(num_q_heads / num_kv_heads);
+    const int log2_page = log2_of(page_size);
+    const int64_t pages_per_chunk = ((int64_t(1) << pl.log2_chunk) >> log2_page) + 1;
+
+    Params p{};
+    p.q = q;
+    p.k = k_cache;
+    p.v = v_cache;
+    p.table = block_table;
+    p.lens = seq_lens;
+    p.out = out;
+    p.part_acc = pl.ws_bytes ? static_cast<float*>(workspace) : nullptr;
+    p.part_ml = pl.ws_bytes ? reinterpret_cast<float2*>(static_cast<char*>(workspace) + pl.ml_offset) : nullptr;
+    p.max_pages = max_pages_per_seq;
+    p.page_stride = (uint32_t)(num_kv_heads * page_size * head_dim);
+    p.num_pages = (int32_t)num_pages;
+    p.hq = (int32_t)num_q_heads;
+    p.hkv = (int32_t)num_kv_heads;
+    p.log2_page = log2_page;
+    p.log2_chunk = pl.log2_chunk;
+    p.splits = (int32_t)pl.splits;
+    p.max_seq_len = (int32_t)max_seq_len;
+    p.pages_lds = (int32_t)((pages_per_chunk * 4 + 15) / 16 * 16);
+    p.c = (float)((double)scale * 1.4426950408889634);  // log2(e)
+
+    (void)hipGetLastError();
+    const hipError_t e = launch(p, group, num_seqs, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return err(WQ_ERR_HIP, "%s: HIP error %d (%s)", fn, (int)e, hipGetErrorString(e));
+    return WQ_OK;
+}
+
+}  // extern "C"

@@ -5,7 +5,13 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "wq.h"
+
 namespace wq {
+
+// Records `message` as the calling thread's last error message (the one
+// wq_last_error_message returns) and returns `st`.
+wq_status record_error(wq_status st, const char* message);
 
 // Quantize + pack: one thread per (row, group).
 hipError_t launch_pack(const float* w, uint32_t* packed, uint16_t* scales,

@@ -1,4 +1,4 @@
-"""Thin ctypes binding of the C ABI in include/wq.h.
+"""Thin ctypes binding of the C ABI in include/wq.h and include/wq_attention.h.
 
 Only argument marshalling happens here: torch tensors are turned into device
 pointers and sizes, the current HIP stream is passed through, and non-OK
@@ -22,9 +22,9 @@ WQ_ERR_HIP = 4
 
 GROUP = 32
 
-# Every function declared in include/wq.h.
+# Every function declared in the headers under include/.
 EXPORTED = ("wq_status_string", "wq_last_error_message", "wq_version", "wq_pack", "wq_gemv",
-            "wq_decode_linears")
+            "wq_decode_linears", "wq_paged_attention_workspace_size", "wq_paged_attention")
 
 
 class WqLinear(ctypes.Structure):
@@ -69,6 +69,11 @@ def lib() -> ctypes.CDLL:
     L.wq_gemv.restype = ctypes.c_int
     L.wq_decode_linears.argtypes = [ctypes.POINTER(WqLinear), i64, i64, i64, vp]
     L.wq_decode_linears.restype = ctypes.c_int
+    L.wq_paged_attention_workspace_size.argtypes = [i64, i64, i64, i64, i64, ctypes.POINTER(ctypes.c_size_t)]
+    L.wq_paged_attention_workspace_size.restype = ctypes.c_int
+    L.wq_paged_attention.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, i64, i64, i64,
+                                     ctypes.c_float, vp, ctypes.c_size_t, vp]
+    L.wq_paged_attention.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -176,3 +181,55 @@ def wq_decode_linears(linears, m: int = 1, group: int = GROUP, stream=None, _arr
     arr = _array if _array is not None else make_linear_array(linears, m, group)
     device = linears[0][2].device
     _check(lib().wq_decode_linears(arr, len(arr), m, group, _stream(stream, device)))
+
+
+# ------------------------------------------------------- paged attention
+
+def paged_attention_workspace_size(num_seqs: int, num_q_heads: int, num_kv_heads: int,
+                                   head_dim: int, max_seq_len: int) -> int:
+    """Bytes of device workspace wq_paged_attention needs (0: none)."""
+    out = ctypes.c_size_t(0)
+    _check(lib().wq_paged_attention_workspace_size(num_seqs, num_q_heads, num_kv_heads, head_dim,
+                                                   max_seq_len, ctypes.byref(out)))
+    return int(out.value)
+
+
+def paged_workspace(q, max_seq_len: int, num_kv_heads: int):
+    """A device workspace (uint8 tensor, or None) sized for these shapes."""
+    import torch
+
+    num_seqs, hq, d = q.shape
+    n = paged_attention_workspace_size(num_seqs, hq, num_kv_heads, d, max_seq_len)
+    return torch.empty(n, dtype=torch.uint8, device=q.device) if n else None
+
+
+def paged_attention(q, k_cache, v_cache, block_table, seq_lens, out, scale: float, max_seq_len: int,
+                    workspace=None, stream=None) -> None:
+    """out [S, HQ, D] = decode attention of q [S, HQ, D] over the paged
+    caches [pages, HKV, P, D] (fp16), block_table [S, max_pages] and
+    seq_lens [S] (int32), all on one device.  `workspace` is a uint8 device
+    tensor from paged_workspace (allocated here when omitted)."""
+    import torch
+
+    if q.dim() != 3 or k_cache.dim() != 4:
+        raise ValueError("q must be [S, HQ, D] and the caches [pages, HKV, P, D]")
+    num_seqs, hq, d = q.shape
+    num_pages, hkv, page, d2 = k_cache.shape
+    max_pages = block_table.shape[1] if block_table.dim() == 2 else 0
+    pq = _dev_tensor(q, "q", _half_dtypes(), (num_seqs, hq, d))
+    pk = _dev_tensor(k_cache, "k_cache", _half_dtypes(), (num_pages, hkv, page, d2))
+    pv = _dev_tensor(v_cache, "v_cache", _half_dtypes(), (num_pages, hkv, page, d2))
+    pt = _dev_tensor(block_table, "block_table", (torch.int32,), (num_seqs, max_pages))
+    pl = _dev_tensor(seq_lens, "seq_lens", (torch.int32,), (num_seqs,))
+    po = _dev_tensor(out, "out", _half_dtypes(), (num_seqs, hq, d))
+    if workspace is None:
+        workspace = paged_workspace(q, max_seq_len, hkv)
+    if workspace is not None:
+        if workspace.device != q.device or workspace.dtype != torch.uint8 or not workspace.is_contiguous():
+            raise ValueError("workspace must be a contiguous uint8 tensor on the device of q")
+        pw, nw = ctypes.c_void_p(workspace.data_ptr()), workspace.numel()
+    else:
+        pw, nw = None, 0
+    _check(lib().wq_paged_attention(pq, pk, pv, pt, pl, po, num_seqs, hq, hkv, d, page, num_pages,
+                                    max_pages, max_seq_len, float(scale), pw, nw,
+                                    _stream(stream, q.device)))

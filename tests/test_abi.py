@@ -1,5 +1,5 @@
 """The C-ABI library on the CPU: it loads, exports every function declared in
-include/wq.h, and rejects invalid arguments on the host before any HIP call
+the headers under include/, and rejects invalid arguments on the host before any HIP call
 (no GPU needed: these calls never reach the device)."""
 
 import ctypes
@@ -11,7 +11,8 @@ import sys
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "wq.h")
+HEADERS = sorted(os.path.join(ROOT, "include", f) for f in os.listdir(os.path.join(ROOT, "include"))
+                 if f.endswith(".h"))
 
 
 @pytest.fixture(scope="module")
@@ -26,7 +27,7 @@ def L():
 
 
 def declared_functions():
-    src = open(HEADER).read()
+    src = "".join(open(h).read() for h in HEADERS)
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
     return sorted(set(re.findall(r"\b(wq_[a-z_]+)\s*\(", src)))
 
@@ -177,3 +178,64 @@ def test_binding_refuses_host_tensors():
     w = torch.zeros(4, 32)
     with pytest.raises(ValueError, match="device tensor"):
         wq.wq_pack(w, torch.zeros(4, 4, dtype=torch.int32), torch.zeros(4, 1, dtype=torch.float16))
+
+
+# ------------------------------------------------------- paged attention
+
+QA, KA, VA, TA, LA, OA, WA = (0x1000000 * i for i in range(1, 8))
+
+
+def attention(L, q=QA, k=KA, v=VA, t=TA, lens=LA, o=OA, seqs=1, hq=24, hkv=8, d=128, page=16, pages=256,
+              max_pages=256, max_len=4096, scale=0.088, ws=WA, ws_bytes=1 << 24):
+    return L.wq_paged_attention(vp(q), vp(k), vp(v), vp(t), vp(lens), vp(o), seqs, hq, hkv, d, page, pages,
+                                max_pages, max_len, scale, vp(ws), ws_bytes, None)
+
+
+def workspace_bytes(L, seqs, hq, hkv, d, max_len):
+    out = ctypes.c_size_t(12345)
+    st = L.wq_paged_attention_workspace_size(seqs, hq, hkv, d, max_len, ctypes.byref(out))
+    return st, out.value
+
+
+@pytest.mark.parametrize(
+    "kwargs,status,needle",
+    [
+        (dict(q=0), 1, "null"), (dict(k=0), 1, "null"), (dict(v=0), 1, "null"),
+        (dict(t=0), 1, "null"), (dict(lens=0), 1, "null"), (dict(o=0), 1, "null"),
+        (dict(seqs=0), 1, "num_seqs"), (dict(seqs=(1 << 20) + 1), 1, "num_seqs"),
+        (dict(hkv=0), 1, "num_kv_heads"), (dict(hkv=257, hq=257), 1, "num_kv_heads"),
+        (dict(hq=20), 1, "multiple"), (dict(hq=72), 2, "query heads per kv head"),
+        (dict(d=64), 2, "head_dim"), (dict(page=12), 2, "page_size"), (dict(page=2048), 2, "page_size"),
+        (dict(page=0), 2, "page_size"), (dict(pages=0), 1, "num_pages"), (dict(max_pages=0), 1, "max_pages"),
+        (dict(max_len=-1), 1, "max_seq_len"), (dict(max_len=(1 << 22) + 1, max_pages=1 << 20), 1, "max_seq_len"),
+        (dict(max_len=4097), 1, "exceeds"), (dict(scale=float("inf")), 1, "scale"),
+        (dict(scale=float("nan")), 1, "scale"),
+        (dict(q=QA + 8), 3, "16-byte"), (dict(o=OA + 2), 3, "16-byte"), (dict(k=KA + 4), 3, "16-byte"),
+        (dict(v=VA + 8), 3, "16-byte"), (dict(t=TA + 2), 3, "4-byte"), (dict(lens=LA + 1), 3, "4-byte"),
+        (dict(ws=0), 1, "workspace"), (dict(ws_bytes=1000), 1, "workspace"), (dict(ws=WA + 4), 3, "workspace"),
+        (dict(o=QA + 64), 1, "out overlaps"), (dict(o=KA + 4096), 1, "out overlaps"),
+        (dict(o=LA), 1, "out overlaps"), (dict(ws=TA), 1, "workspace overlaps"),
+        (dict(o=WA + 256), 1, "out overlaps the workspace"),
+    ],
+)
+def test_attention_rejects(L, kwargs, status, needle):
+    st = attention(L, **kwargs)
+    assert st == status, L.wq_last_error_message()
+    assert needle in L.wq_last_error_message().decode()
+
+
+def test_attention_workspace_size(L):
+    # one sequence of 4096 tokens, 8 kv heads: 64 chunks of 64 tokens, so
+    # per query head 64 x (128 floats + (m, l))
+    assert workspace_bytes(L, 1, 24, 8, 128, 4096) == (0, 24 * 64 * (128 * 4 + 8))
+    # a short sequence is not split: no workspace
+    assert workspace_bytes(L, 1, 24, 8, 128, 64) == (0, 0)
+    assert workspace_bytes(L, 1, 24, 8, 128, 0) == (0, 0)
+    # many sequences: chunks grow so the launch stays near 1024 workgroups
+    st, n = workspace_bytes(L, 64, 32, 8, 128, 4096)
+    assert st == 0 and n == 64 * 32 * 2 * (128 * 4 + 8)
+    assert workspace_bytes(L, 1, 24, 8, 64, 4096)[0] == 2
+    assert L.wq_paged_attention_workspace_size(1, 24, 8, 128, 4096, None) == 1
+    # the call accepts exactly the reported size and no less
+    n = workspace_bytes(L, 1, 24, 8, 128, 4096)[1]
+    assert attention(L, ws_bytes=n - 1) == 1
