@@ -42,6 +42,12 @@ def parse_args():
                     help="also time the step with every linear reading its predecessor's output")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (for scaling HBM counters)")
+    ap.add_argument("--attention-only", action="store_true",
+                    help="time only the paged decode-attention shapes (for profiling its kernels)")
+    ap.add_argument("--attention-config", type=int, default=None,
+                    help="with --attention-only: time only this entry of ATTN_CONFIGS")
+    ap.add_argument("--attention-eager", action="store_true",
+                    help="with --attention-only: launch every call from the host (no HIP graph)")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the per-shape figures (single linears, small batches, 8B-class step)")
     return ap.parse_args()
@@ -253,6 +259,113 @@ def time_pack(n, k, gen, device, calls=10):
     return [round(ms * 1e3, 2), round(nbytes / (ms * 1e-3) / 1e9, 1)]
 
 
+def time_attention_rotated(hq, hkv, lens, page, seed, device, calls=256, reps=5, eager=False):
+    """Per-call time of wq_paged_attention, cold: the calls rotate over
+    per-layer caches totalling >= 1 GiB (each layer's K and V arrays hold the
+    same sequences under one shared block table, as in a decode step) and are
+    replayed from a HIP graph.  Returns (us per call, GB/s, bytes per call)."""
+    import torch
+
+    from paper_2412_15803_amd import attn_workloads as aw
+    from paper_2412_15803_amd import wq
+
+    per = aw.attention_bytes(lens, hq, hkv, aw.HEAD_DIM, page)
+    r = max(1, -(-(1 << 30) // per))
+    need = aw.pages_needed(lens, page)
+    k_all, v_all = aw.kv_cache_device(seed, r * need, hkv, page, aw.HEAD_DIM, device=device)
+    layers = [(k_all[i * need:(i + 1) * need], v_all[i * need:(i + 1) * need]) for i in range(r)]
+    table_np, _ = aw.block_table_host(seed + 1, lens, page)
+    table = torch.from_numpy(table_np).to(device)
+    lens_t = torch.tensor(lens, dtype=torch.int32, device=device)
+    q = aw.q_device(seed + 2, len(lens), hq, aw.HEAD_DIM, device=device)
+    out = torch.empty_like(q)
+    ml = max(lens)
+    ws = wq.paged_workspace(q, ml, hkv)
+    scale = aw.default_scale(aw.HEAD_DIM)
+
+    def call(i, dst):
+        k, v = layers[i % r]
+        wq.paged_attention(q, k, v, table, lens_t, dst, scale, ml, workspace=ws)
+
+    side = torch.cuda.Stream(device)
+    side.wait_stream(torch.cuda.current_stream(device))
+    with torch.cuda.stream(side):
+        for i in range(3):
+            call(i, out)
+    torch.cuda.current_stream(device).wait_stream(side)
+    torch.cuda.synchronize()
+    ref = torch.empty_like(out)
+    call(calls - 1, ref)
+    graph = None
+    if not eager:
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for i in range(calls):
+                call(i, out)
+    times = []
+    for _ in range(reps):
+        a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        if graph is not None:
+            graph.replay()
+        else:
+            for i in range(calls):
+                call(i, out)
+        e.record()
+        torch.cuda.synchronize()
+        times.append(a.elapsed_time(e) / calls)
+        if not torch.equal(out, ref):
+            raise RuntimeError(f"repeated wq_paged_attention {lens[:2]} differs from the first call")
+    ms = sorted(times)[len(times) // 2]
+    del graph, layers, k_all, v_all
+    torch.cuda.empty_cache()
+    return round(ms * 1e3, 2), round(per / (ms * 1e-3) / 1e9, 1), per
+
+
+# Counter summaries of the split kernel, by ATTN_CONFIGS index.
+ATTN_PROFILES = {0: "paged_attention_3b_ctx4096.md", 1: "paged_attention_3b_ctx32768.md"}
+ATTN_SOURCES = ("wq_attention.hip", "wq_device.h")
+
+
+def attention_traffic(index):
+    """HBM bytes per split-kernel launch from the committed counter summary of
+    this attention shape, or None (no summary, or the kernel changed since)."""
+    from paper_2412_15803_amd.build import source_hash
+    from paper_2412_15803_amd.profsum import parse_traffic
+
+    name = ATTN_PROFILES.get(index)
+    got = parse_traffic(os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", name)) if name else None
+    if not got or got[0] != source_hash(ATTN_SOURCES):
+        return None
+    return int(got[1])
+
+
+ATTN_CONFIGS = (
+    # (label, query heads, kv heads, sequence lengths); pages of 16 tokens
+    ("3B attention, 1 sequence of 4096 tokens", 24, 8, (4096,)),
+    ("3B attention, 1 sequence of 32768 tokens", 24, 8, (32768,)),
+    ("3B attention, 16 sequences of 4096 tokens", 24, 8, (4096,) * 16),
+    ("8B attention, 1 sequence of 4096 tokens", 32, 8, (4096,)),
+    ("8B attention, 1 sequence of 32768 tokens", 32, 8, (32768,)),
+)
+
+
+def attention_configs(device, seed, only=None, eager=False):
+    """Decode attention over a paged cache (24 or 32 query heads, 8 kv heads
+    of 128, pages of 16 tokens): device time per call, GB/s of cached keys
+    and values (plus q, out, table) and the fraction of the HBM peak."""
+    how = "launched one by one from the host" if eager else "replayed from a HIP graph (device time per call)"
+    res = {"method": "wq_paged_attention calls (split and merge kernels) rotated over >= 1 GiB of per-layer "
+                     f"caches sharing one block table, {how}"}
+    for i, (label, hq, hkv, lens) in enumerate(ATTN_CONFIGS):
+        if only is not None and i != only:
+            continue
+        us, gbs, per = time_attention_rotated(hq, hkv, lens, 16, seed + 100 + i, device, eager=eager)
+        res[label] = {"us": us, "GB_s": gbs, "frac": round(gbs / HBM_PEAK_GBS, 4), "bytes": per,
+                      "split_kernel_traffic": attention_traffic(i)}
+    return res
+
+
 def per_config(device, seed):
     """Per-shape figures beside the headline step (SURVEY configs 1-4 and the
     8B-class step); none of them is the bench value."""
@@ -279,6 +392,7 @@ def per_config(device, seed):
         res[f"3B step M={m} (one wq_decode_linears call, 113 linears)"] = v
     for m, v in time_step_batches(steps8, [1, 4, 8, 16], gen, device, 20, 3).items():
         res[f"8B step M={m} (one wq_decode_linears call, 129 linears)"] = v
+    res["paged decode attention"] = attention_configs(device, seed)
     return res
 
 
@@ -323,6 +437,14 @@ def main():
         sys.exit(1)
     device = torch.device("cuda:0")
     wq.lib()  # fail loudly if the HIP library is missing
+
+    if args.attention_only:
+        if args.copy_probe_mib:
+            copy_probe(args.copy_probe_mib, device)
+        log("timing the paged decode-attention shapes")
+        res = attention_configs(device, args.seed, args.attention_config, args.attention_eager)
+        print(json.dumps({"paged decode attention": res}), flush=True)
+        return
 
     log("building the 3B-class decode step (113 linears) on the device")
     plan, lins, step_bytes = build_step(args.seed, device)

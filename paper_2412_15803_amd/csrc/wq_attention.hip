@@ -5,7 +5,7 @@
 // one pass over the cache, split along the sequence where one workgroup per
 // head would leave the chip idle.
 //
-// Work split.  A sequence is cut into chunks of T = 2^log2_chunk tokens.  One
+// Work split.  A sequence is cut into chunks of T tokens (a multiple of 64).  One
 // 256-thread workgroup takes one (sequence, kv head, chunk) and serves all G
 // query heads of that kv head, so every cached key and value is read from HBM
 // once.  Each of its four waves takes a contiguous quarter of the chunk.
@@ -54,13 +54,13 @@ constexpr int kWaves = kThreads / 64;
 constexpr int kRowsPerLoad = 4;                              // tokens per wave-wide load
 constexpr int kLoadsPerBlock = 4;
 constexpr int kBlockTokens = kRowsPerLoad * kLoadsPerBlock;  // 16 tokens of one wave
-constexpr int kMinLog2Chunk = 6;                             // 64 tokens: a block per wave
-constexpr int kMaxLog2Chunk = 12;
+constexpr int kChunkQuantum = kWaves * kBlockTokens;        // 64 tokens: a block per wave
+constexpr int kMaxChunk = 4096;
 constexpr int kMaxSplits = 1024;
+static_assert(WQ_ATTN_MAX_SEQ_LEN / kMaxChunk <= kMaxSplits, "chunks per sequence stay bounded");
 constexpr uint16_t kHalfNaN = 0x7E00;
 
 static_assert(kD == 128, "the lane layout assumes 16 lanes x 8 dims per token");
-static_assert((1 << kMinLog2Chunk) == kWaves * kBlockTokens, "a chunk holds whole blocks");
 
 struct Params {
     const uint16_t* q;
@@ -76,10 +76,11 @@ struct Params {
     int32_t num_pages;
     int32_t hq, hkv;
     int32_t log2_page;
-    int32_t log2_chunk;
+    int32_t chunk;            // tokens per chunk, a multiple of kChunkQuantum
     int32_t splits;
     int32_t max_seq_len;
-    int32_t pages_lds;  // bytes of LDS before the wave states
+    int32_t pages_per_chunk;  // block-table entries one chunk can use
+    int32_t pages_lds;        // bytes of LDS before the wave states
     float c;            // scale * log2(e): scores in log2 units
 };
 
@@ -151,21 +152,17 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const Params p) {
     const int s = seq_kv / p.hkv;
     const int64_t head0 = (int64_t)s * p.hq + (int64_t)kvh * G;  // first query head of the group
 
-    const int len = p.lens[s];
-    if (bad_length(p, len) || len == 0) {
-        if (p.splits == 1) {
-            const uint16_t fill = len == 0 ? 0 : kHalfNaN;
-            for (int i = tid; i < G * kD; i += kThreads) p.out[head0 * kD + i] = fill;
-        }
-        return;
-    }
-    const int c0 = chunk << p.log2_chunk;
-    if (c0 >= len) return;
-
     const int lane = tid & 63, row = lane >> 4, col = lane & 15;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int log2_page = p.log2_page;
+    const int page_mask = (1 << log2_page) - 1;
+    const int c0 = chunk * p.chunk;
+    const int first_page = c0 >> log2_page;
 
-    // The query heads' 8 dims of this lane.
+    // One round trip for the length, the query vectors and the block-table
+    // entries the chunk may use (bounded by the table row: the length is not
+    // known yet).  Entries are checked against the cache size when used.
+    const int len = p.lens[s];
     half2v qv[G][4];
 #pragma unroll
     for (int g = 0; g < G; ++g) {
@@ -175,27 +172,23 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const Params p) {
         qv[g][2] = as_h2(t.z);
         qv[g][3] = as_h2(t.w);
     }
-
-    // Physical pages of the chunk's tokens, checked against the cache size.
-    const int log2_page = p.log2_page;
-    const int page_mask = (1 << log2_page) - 1;
-    const int first_page = c0 >> log2_page;
-    const int cend = min(c0 + (1 << p.log2_chunk), len);
-    const int npages = ((cend - 1) >> log2_page) - first_page + 1;
     const int32_t* trow = p.table + (int64_t)s * p.max_pages + first_page;
-    int bad = 0;
-    for (int i = tid; i < npages; i += kThreads) {
-        int pg = trow[i];
-        if ((uint32_t)pg >= (uint32_t)p.num_pages) {
-            bad = 1;
-            pg = 0;
+    const int table_left = (int)min<int64_t>(p.pages_per_chunk, p.max_pages - first_page);
+    for (int i = tid; i < table_left; i += kThreads) sh_pages[i] = trow[i];
+    __syncthreads();
+
+    if (bad_length(p, len) || len == 0) {
+        if (p.splits == 1) {
+            const uint16_t fill = len == 0 ? 0 : kHalfNaN;
+            for (int i = tid; i < G * kD; i += kThreads) p.out[head0 * kD + i] = fill;
         }
-        sh_pages[i] = pg;
+        return;
     }
-    const int any_bad = __syncthreads_or(bad);
+    if (c0 >= len) return;
+    int bad = 0;
 
     // This wave's tokens: [wbase, wbase + wtok) intersected with [0, len).
-    const int wtok = 1 << (p.log2_chunk - 2);
+    const int wtok = p.chunk / kWaves;
     const int wbase = c0 + wave * wtok;
     const int nvalid = min(max(len - wbase, 0), wtok);
     const int nblk = (nvalid + kBlockTokens - 1) / kBlockTokens;
@@ -207,7 +200,11 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const Params p) {
 #pragma unroll
         for (int j = 0; j < kLoadsPerBlock; ++j) {
             const int t = min(wbase + blk * kBlockTokens + j * kRowsPerLoad + row, len - 1);
-            const uint32_t pg = (uint32_t)sh_pages[(t >> log2_page) - first_page];
+            uint32_t pg = (uint32_t)sh_pages[(t >> log2_page) - first_page];
+            if (pg >= (uint32_t)p.num_pages) {
+                bad = 1;
+                pg = 0;
+            }
             const uint64_t off = (uint64_t)pg * p.page_stride +
                                  (uint64_t)((head_slot0 + (uint32_t)(t & page_mask)) * kD + col * 8);
             b.k[j] = *gbl(reinterpret_cast<const u32x4*>(p.k + off));
@@ -235,9 +232,9 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const Params p) {
                 sc[g][j] = ok ? d * p.c : -INFINITY;
             }
         }
-        float vf[kLoadsPerBlock][8];
-#pragma unroll
-        for (int j = 0; j < kLoadsPerBlock; ++j) unpack8(b.v[j], vf[j]);
+        // Rescale each head's state to the block's new maximum and turn the
+        // scores into weights, then add the weighted values slab by slab (only
+        // one slab's values are unpacked at a time).
 #pragma unroll
         for (int g = 0; g < G; ++g) {
             float mx = st[g].m;
@@ -250,13 +247,20 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const Params p) {
             for (int e = 0; e < 8; ++e) st[g].acc[e] *= corr;
 #pragma unroll
             for (int j = 0; j < kLoadsPerBlock; ++j) {
-                const float pj = exp2_(sc[g][j] - ms);
-                l += pj;
-#pragma unroll
-                for (int e = 0; e < 8; ++e) st[g].acc[e] = fmaf(pj, vf[j][e], st[g].acc[e]);
+                sc[g][j] = exp2_(sc[g][j] - ms);
+                l += sc[g][j];
             }
             st[g].l = l;
             st[g].m = mx;
+        }
+#pragma unroll
+        for (int j = 0; j < kLoadsPerBlock; ++j) {
+            float vf[8];
+            unpack8(b.v[j], vf);
+#pragma unroll
+            for (int g = 0; g < G; ++g)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) st[g].acc[e] = fmaf(sc[g][j], vf[e], st[g].acc[e]);
         }
     };
 
@@ -301,7 +305,7 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const Params p) {
             }
         }
     }
-    __syncthreads();
+    const int any_bad = __syncthreads_or(bad);
     for (int i = tid; i < G * kD; i += kThreads) {
         const int g = i / kD, d = i % kD;
         float mx = -INFINITY;
@@ -324,96 +328,98 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const Params p) {
     }
 }
 
-__device__ __forceinline__ float block_max(float v, float* sh) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-    if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
-    __syncthreads();
-    float r = sh[0];
-#pragma unroll
-    for (int w = 1; w < kWaves; ++w) r = fmaxf(r, sh[w]);
-    return r;
-}
-
-__device__ __forceinline__ float block_sum(float v, float* sh) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-    if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
-    __syncthreads();
-    float r = sh[0];
-#pragma unroll
-    for (int w = 1; w < kWaves; ++w) r += sh[w];
-    return r;
-}
-
 // One workgroup per (sequence, query head): out = sum_c 2^(m_c - M) acc_c /
-// sum_c 2^(m_c - M) l_c over the sequence's chunks, M = max_c m_c.
+// sum_c 2^(m_c - M) l_c over the sequence's chunks, M = max_c m_c.  Thread
+// (slot, col) folds chunks slot, slot + 8, ... of dims 4 col .. 4 col + 3
+// into a running state; the first batch of chunk loads is issued together
+// with the length (only chunks below the launch's split count, all inside
+// the workspace), so short sequences take one round trip.  The eight slot
+// states are then merged through LDS.
 __global__ __launch_bounds__(kThreads) void merge_kernel(const Params p) {
-    constexpr int kSlots = kThreads / (kD / 4);  // 8 chunk slots x 32 four-dim columns
-    __shared__ float sh_w[kMaxSplits];
-    __shared__ float sh_red[2][kWaves];
-    __shared__ float4 sh_part[kSlots][kD / 4];
+    constexpr int kCols = kD / 4;             // 32 four-dim columns
+    constexpr int kSlots = kThreads / kCols;  // 8 chunk slots
+    constexpr int kBatch = 8;                 // chunks per slot loaded at once
+    __shared__ float sh_m[kSlots], sh_l[kSlots];
+    __shared__ float4 sh_a[kSlots][kCols];
 
     const int tid = threadIdx.x;
+    const int slot = tid / kCols, cq = tid % kCols;
     const int64_t head = blockIdx.x;  // seq * hq + h
     const int s = (int)(head / p.hq);
     uint16_t* o = p.out + head * kD;
+    const float2* ml = p.part_ml + head * p.splits;
+    const float4* pa = reinterpret_cast<const float4*>(p.part_acc + head * p.splits * kD) + cq;
+
     const int len = p.lens[s];
+    float m = -INFINITY, l = 0.0f;
+    float4 a = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    int n = p.splits;  // chunks that hold data; known once the length arrives
+    for (int base = slot; base < n; base += kSlots * kBatch) {
+        float2 h[kBatch];
+        float4 v[kBatch];
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+            const int c = min(base + j * kSlots, p.splits - 1);
+            h[j] = ml[c];
+            v[j] = pa[(int64_t)c * kCols];
+        }
+        if (base == slot) {
+            if (bad_length(p, len) || len == 0) break;
+            n = (len + p.chunk - 1) / p.chunk;
+        }
+        float mx = m;
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j)
+            if (base + j * kSlots < n) mx = fmaxf(mx, h[j].x);
+        if (mx == -INFINITY) break;  // no chunk of this slot holds data
+        const float corr = exp2_(m - mx);
+        l *= corr;
+        a.x *= corr;
+        a.y *= corr;
+        a.z *= corr;
+        a.w *= corr;
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+            if (base + j * kSlots >= n) continue;
+            const float w = exp2_(h[j].x - mx);
+            l = fmaf(h[j].y, w, l);
+            a.x = fmaf(w, v[j].x, a.x);
+            a.y = fmaf(w, v[j].y, a.y);
+            a.z = fmaf(w, v[j].z, a.z);
+            a.w = fmaf(w, v[j].w, a.w);
+        }
+        m = mx;
+    }
     if (bad_length(p, len) || len == 0) {
         if (tid < kD) o[tid] = len == 0 ? 0 : kHalfNaN;
         return;
     }
-    const int n = (len + (1 << p.log2_chunk) - 1) >> p.log2_chunk;
-    const float2* ml = p.part_ml + head * p.splits;
-    const float4* pa = reinterpret_cast<const float4*>(p.part_acc + head * p.splits * kD);
-
-    constexpr int kPer = kMaxSplits / kThreads;
-    float2 hdr[kPer];
-    float mx = -INFINITY;
-#pragma unroll
-    for (int r = 0; r < kPer; ++r) {
-        const int c = tid + r * kThreads;
-        hdr[r] = c < n ? ml[c] : make_float2(-INFINITY, 0.0f);
-        mx = fmaxf(mx, hdr[r].x);
+    if (cq == 0) {
+        sh_m[slot] = m;
+        sh_l[slot] = l;
     }
-    mx = block_max(mx, sh_red[0]);
-    float l = 0.0f;
-#pragma unroll
-    for (int r = 0; r < kPer; ++r) {
-        const int c = tid + r * kThreads;
-        if (c < n) {
-            const float w = exp2_(hdr[r].x - mx);
-            sh_w[c] = w;
-            l = fmaf(hdr[r].y, w, l);
-        }
-    }
-    l = block_sum(l, sh_red[1]);  // its barrier also publishes sh_w
-
-    const int slot = tid / (kD / 4), dq = tid % (kD / 4);
-    float4 a = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-    for (int c = slot; c < n; c += kSlots) {
-        const float w = sh_w[c];
-        const float4 v = pa[c * (kD / 4) + dq];
-        a.x = fmaf(w, v.x, a.x);
-        a.y = fmaf(w, v.y, a.y);
-        a.z = fmaf(w, v.z, a.z);
-        a.w = fmaf(w, v.w, a.w);
-    }
-    sh_part[slot][dq] = a;
+    sh_a[slot][cq] = a;
     __syncthreads();
     if (tid < kD) {
-        const float* col = reinterpret_cast<const float*>(&sh_part[0][0]) + tid;
-        float acc = 0.0f;
+        float mx = -INFINITY;
 #pragma unroll
-        for (int sl = 0; sl < kSlots; ++sl) acc += col[sl * kD];
-        o[tid] = to_half_bits(acc / l);
+        for (int sl = 0; sl < kSlots; ++sl) mx = fmaxf(mx, sh_m[sl]);
+        const float* col = reinterpret_cast<const float*>(&sh_a[0][0]) + tid;
+        float lt = 0.0f, acc = 0.0f;
+#pragma unroll
+        for (int sl = 0; sl < kSlots; ++sl) {
+            const float w = exp2_(sh_m[sl] - mx);
+            lt = fmaf(sh_l[sl], w, lt);
+            acc = fmaf(col[sl * kD], w, acc);
+        }
+        o[tid] = to_half_bits(acc / lt);
     }
 }
 
 // ------------------------------------------------------------------- host
 
 struct Plan {
-    int log2_chunk;
+    int64_t chunk;
     int64_t splits;
     size_t ml_offset;  // bytes of part_acc
     size_t ws_bytes;
@@ -422,19 +428,20 @@ struct Plan {
 int64_t target_blocks() {
     const char* e = getenv("WQ_ATTN_TARGET_BLOCKS");
     const long v = e ? strtol(e, nullptr, 10) : 0;
-    return v > 0 ? v : 1024;
+    return v > 0 ? v : 512;
 }
 
-// Chunk length: the smallest power of two from 64 tokens that keeps the
-// split launch within about target_blocks() workgroups and the chunks of a
-// sequence within kMaxSplits.
+// Chunk length: a multiple of 64 tokens that gives the split launch about
+// target_blocks() workgroups (what the chip holds at once, so there is a
+// single round of them), at most kMaxChunk tokens; with sequences of at most
+// WQ_ATTN_MAX_SEQ_LEN tokens that keeps a sequence within kMaxSplits chunks.
 Plan make_plan(int64_t seqs, int64_t hq, int64_t hkv, int64_t max_seq_len) {
     const int64_t len = std::max<int64_t>(max_seq_len, 1);
-    auto splits_of = [&](int lc) { return (len + (int64_t(1) << lc) - 1) >> lc; };
-    const int64_t target = target_blocks();
-    int lc = kMinLog2Chunk;
-    while (lc < kMaxLog2Chunk && (splits_of(lc) > kMaxSplits || seqs * hkv * splits_of(lc) > target)) ++lc;
-    Plan pl{lc, splits_of(lc), 0, 0};
+    const int64_t want = std::max<int64_t>(1, target_blocks() / (seqs * hkv));  // chunks per sequence
+    int64_t chunk = (len + want - 1) / want;
+    chunk = (chunk + kChunkQuantum - 1) / kChunkQuantum * kChunkQuantum;
+    chunk = std::min<int64_t>(std::max<int64_t>(chunk, kChunkQuantum), kMaxChunk);
+    Plan pl{chunk, (len + chunk - 1) / chunk, 0, 0};
     if (pl.splits > 1) {
         pl.ml_offset = (size_t)(seqs * hq * pl.splits * kD * 4);
         pl.ws_bytes = pl.ml_offset + (size_t)(seqs * hq * pl.splits * 8);
@@ -589,7 +596,8 @@ wq_status wq_paged_attention(const uint16_t* q, const uint16_t* k_cache, const u
 
     const int group = (int)(num_q_heads / num_kv_heads);
     const int log2_page = log2_of(page_size);
-    const int64_t pages_per_chunk = ((int64_t(1) << pl.log2_chunk) >> log2_page) + 1;
+    // Pages a chunk can touch: it may start inside a page.
+    const int64_t pages_per_chunk = (pl.chunk >> log2_page) + 2;
 
     Params p{};
     p.q = q;
@@ -606,9 +614,10 @@ wq_status wq_paged_attention(const uint16_t* q, const uint16_t* k_cache, const u
     p.hq = (int32_t)num_q_heads;
     p.hkv = (int32_t)num_kv_heads;
     p.log2_page = log2_page;
-    p.log2_chunk = pl.log2_chunk;
+    p.chunk = (int32_t)pl.chunk;
     p.splits = (int32_t)pl.splits;
     p.max_seq_len = (int32_t)max_seq_len;
+    p.pages_per_chunk = (int32_t)pages_per_chunk;
     p.pages_lds = (int32_t)((pages_per_chunk * 4 + 15) / 16 * 16);
     p.c = (float)((double)scale * 1.4426950408889634);  // log2(e)
 

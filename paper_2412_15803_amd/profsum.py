@@ -44,24 +44,39 @@ def _copy_value(entries):
     return max(copies)
 
 
-def summarise(args):
-    trace = [r for r in _rows(args.trace, "*kernel_trace.csv") if args.kernel in r["Kernel_Name"]]
+def _durations(trace_dir, kernel):
+    trace = [r for r in _rows(trace_dir, "*kernel_trace.csv") if kernel in r["Kernel_Name"]]
     if not trace:
-        raise SystemExit(f"kernel {args.kernel!r} not in the trace")
-    durs = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in trace]
+        raise SystemExit(f"kernel {kernel!r} not in the trace")
+    return [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in trace]
+
+
+def _traffic(fetch, write, f_scale, w_scale, kernel):
+    kf = [v for name, _, v in fetch if kernel in name]
+    kw = [v for name, _, v in write if kernel in name]
+    if not kf or not kw:
+        raise SystemExit(f"kernel {kernel!r} not in the counter runs")
+    return kf, kw, statistics.mean(kf) * f_scale * 1024.0, statistics.mean(kw) * w_scale * 1024.0
+
+
+def summarise(args):
+    durs = _durations(args.trace, args.kernel)
     fetch = _counter(args.fetch, "FETCH_SIZE")
     write = _counter(args.write, "WRITE_SIZE")
     copy_kib = args.copy_mib * 1024.0
     f_scale = copy_kib / _copy_value(fetch)
     w_scale = copy_kib / _copy_value(write)
-    kf = [v for name, _, v in fetch if args.kernel in name]
-    kw = [v for name, _, v in write if args.kernel in name]
-    if not kf or not kw:
-        raise SystemExit(f"kernel {args.kernel!r} not in the counter runs")
-    fetch_b = statistics.mean(kf) * f_scale * 1024.0
-    write_b = statistics.mean(kw) * w_scale * 1024.0
+    kf, kw, fetch_b, write_b = _traffic(fetch, write, f_scale, w_scale, args.kernel)
     traffic = fetch_b + write_b
     avg = statistics.mean(durs)
+    others = []
+    for k in args.also or ():
+        d = _durations(args.trace, k)
+        _, _, fb, wb = _traffic(fetch, write, f_scale, w_scale, k)
+        others.append(f"| other kernel `{k}`: launches, avg duration (us), scaled fetch + write bytes | "
+                      f"{len(d)}, {statistics.mean(d):.2f}, {fb:,.0f} + {wb:,.0f} |")
+    names = tuple(args.sources.split(",")) if args.sources else None
+    src_hash = source_hash(names) if names else source_hash()
     lines = [
         f"# {args.title}",
         "",
@@ -85,11 +100,12 @@ def summarise(args):
         f"| scale factors applied (fetch / write) | {f_scale:.4f} / {w_scale:.4f} |",
         f"| HBM traffic per launch, scaled (fetch + write bytes) | {fetch_b:,.0f} + {write_b:,.0f} = {traffic:,.0f} |",
         f"| traffic / algorithmic bytes | {traffic / args.algo_bytes:.4f} |",
+        *others,
         "",
         "Machine-readable (read by bench.py; valid only for this source hash):",
         "",
         "```",
-        f"source_hash: {source_hash()}",
+        f"source_hash: {src_hash}",
         f"traffic_bytes_per_launch: {traffic:.0f}",
         f"avg_duration_us: {avg:.3f}",
         "```",
@@ -127,6 +143,9 @@ def main():
     ap.add_argument("--copy-mib", type=int, required=True)
     ap.add_argument("--command", action="append", required=True)
     ap.add_argument("--title", default="Kernel trace and HBM traffic")
+    ap.add_argument("--also", action="append", help="another kernel to list (durations and traffic)")
+    ap.add_argument("--sources", default=None,
+                    help="comma-separated csrc/ files whose hash marks the summary (default: the step kernel's)")
     ap.add_argument("--out", required=True)
     summarise(ap.parse_args())
 

@@ -231,9 +231,11 @@ def test_attention_workspace_size(L):
     # a short sequence is not split: no workspace
     assert workspace_bytes(L, 1, 24, 8, 128, 64) == (0, 0)
     assert workspace_bytes(L, 1, 24, 8, 128, 0) == (0, 0)
-    # many sequences: chunks grow so the launch stays near 1024 workgroups
-    st, n = workspace_bytes(L, 64, 32, 8, 128, 4096)
-    assert st == 0 and n == 64 * 32 * 2 * (128 * 4 + 8)
+    # more sequences: longer chunks keep the launch near 512 workgroups
+    st, n = workspace_bytes(L, 16, 32, 8, 128, 4096)
+    assert st == 0 and n == 16 * 32 * 4 * (128 * 4 + 8)
+    # enough sequences to fill the chip: no split, no workspace
+    assert workspace_bytes(L, 64, 32, 8, 128, 4096) == (0, 0)
     assert workspace_bytes(L, 1, 24, 8, 64, 4096)[0] == 2
     assert L.wq_paged_attention_workspace_size(1, 24, 8, 128, 4096, None) == 1
     # the call accepts exactly the reported size and no less

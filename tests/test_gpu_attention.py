@@ -88,6 +88,9 @@ RANDOM_CASES = [
     (24, 8, 256, (3000,), None),
     (24, 8, 1024, (2500,), None),
     (24, 8, 16, tuple(range(1, 40)), None),
+    # chunks (multiples of 64 tokens) that start inside a page
+    (24, 8, 256, (20000,), None),
+    (8, 8, 128, (10000,), None),
     (32, 8, 16, (8192,) * 4, None),
     # many sequences: chunks of 512 and 4096 tokens (long per-wave loops,
     # page lists longer than the workgroup)
