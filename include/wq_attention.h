@@ -29,7 +29,7 @@
  * Numerics: scores, softmax and the weighted sum are computed in fp32; each
  * output is rounded once to fp16.  Per element the result is within
  * 2e-3 * sum_t w_t |V_t[d]| + 1e-6 of the exactly rounded value when
- * scale * sum_d |q[d] K_t[d]| <= 100 for every token.
+ * scale * sum_d |q[d] K_t[d]| <= 60 for every token.
  *
  * Because seq_lens and block_table live on the device they cannot be
  * checked before the launch.  The kernels never read outside the arrays

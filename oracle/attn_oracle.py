@@ -28,16 +28,20 @@ from __future__ import annotations
 import numpy as np
 
 # Tolerance for a result computed with fp32 arithmetic (any summation order,
-# any split of the sequence), measured against sum_t w_t |V_t[d]|:
-#   * both sides round to fp16 once: at most 2 * 2^-11 of |o| <= that sum;
-#   * fp32 scores carry a relative weight error below 2 ln2 * 2^-24 * D * S
-#     with S = max_t scale * sum_d |q_d K_t,d| (<= 1.1e-4 at S <= 100, D = 128);
-#   * fp32 sums of p_t V_t and p_t over at most 2^16 terms per chunk level.
-# 2e-3 covers the sum of these with margin while S <= 100 (checked by
-# score_bound() in the tests).  The absolute term covers fp16 subnormals.
+# any split of the sequence), measured against W = sum_t w_t |V_t[d]|:
+#   * both sides round to fp16 once: together at most 2^-10 |o| <= 2^-10 W;
+#   * an fp32 score (a D-term dot product, then one multiply by an fp32
+#     constant) is off by at most (D + 2) 2^-24 S in log units, with
+#     S = max_t scale * sum_d |q_d K_t,d|, so each weight is off by a factor
+#     within 1 +- eps, eps <= (D + 2) 2^-24 S, and the output by <= 2 eps W;
+#   * fp32 sums of p_t V_t and of p_t (a few hundred terms deep in any order
+#     the kernels use): well below 1e-4 W.
+# With D = 128 the total stays below 2e-3 W while S <= 60, the precondition
+# the tests check (random N(0, 1) inputs give S of about 10).  The absolute
+# term covers fp16 subnormals.
 ATTN_REL_TOL = 2e-3
 ATTN_ABS_TOL = 1e-6
-ATTN_MAX_SCORE_BOUND = 100.0
+ATTN_MAX_SCORE_BOUND = 60.0
 
 
 def _check_inputs(q, k_cache, v_cache, block_table, seq_lens):
