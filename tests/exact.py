@@ -166,3 +166,15 @@ def exact_gemv_fp16_bits(codes, scale_bits, x_bits):
             total = sum((w_hat[kk] * xs[mi][kk] for kk in range(k)), Fraction(0))
             out[mi][r] = fraction_to_fp16_bits(round_fp16(total))
     return out
+
+
+def dequant_reference(packed, scale_bits, n: int, k: int) -> np.ndarray:
+    """float64 w_hat [N, K] read through the byte layout: byte t of a row
+    holds element 2t in its low nibble and 2t + 1 in its high nibble; each
+    code q means (q - 8) times its group's fp16 scale."""
+    raw = np.ascontiguousarray(np.asarray(packed, dtype=np.uint32)).view(np.uint8).reshape(n, k // 2)
+    codes = np.empty((n, k), dtype=np.int64)
+    codes[:, 0::2] = raw & 0xF
+    codes[:, 1::2] = raw >> 4
+    s = np.asarray(scale_bits, dtype=np.uint16).view(np.float16).astype(np.float64)
+    return (codes - 8).astype(np.float64) * np.repeat(s, 32, axis=1)
