@@ -1,0 +1,444 @@
+// Decode linears with the elementwise work of a layer fused in (batch 1), and
+// the argmax of the final logits.  The graph-level fusion the paper's compiler
+// performs (Sec. 2.3), written by hand for the Llama-class decoders of
+// Table 1: an RMSNorm or SiLU-gated prologue on x, a residual added to y
+// before its single rounding.
+//
+// fused_m1_kernel<LPR, GPL> is the batch-1 GEMV of wq_kernels.hip (same row
+// steps, buffer loads and two-buffer pipeline) with two changes:
+//   * prologue: the block's 256 threads first compute x_eff for the whole row
+//     into LDS, one round trip for x and the second operand (norm weight or
+//     up half), a fixed-order block sum for RMSNorm, then one fp16 rounding
+//     per element; each wave then stages its lanes' x_eff from LDS;
+//   * epilogue: row sums are staged in LDS as fp32, and the residual is added
+//     when y is written, so y is rounded once.
+// argmax_kernel: one 1024-thread workgroup scans the logits (each thread in
+// increasing index order, strict comparison) and reduces (value, index)
+// pairs with the smaller index winning ties.
+#include <hip/hip_fp16.h>
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <vector>
+
+#include "wq_device.h"
+#include "wq_fused.h"
+#include "wq_internal.h"
+
+namespace wq {
+namespace fused {
+namespace {
+
+using namespace dev;
+
+constexpr int kBlock = 256;
+constexpr int kWavesPerBlock = kBlock / kWave;
+constexpr int kTargetWaves = 256 * 8;
+constexpr int kMaxK = (int)WQ_FUSED_MAX_K;
+constexpr int kChunksPerThread = kMaxK / 8 / kBlock;  // 8-element chunks of x per thread
+constexpr int kArgThreads = 1024;
+
+struct Args {
+    const u32x4* packed;
+    const uint16_t* scales;
+    const uint16_t* x;
+    uint16_t* y;
+    const uint16_t* norm;
+    const uint16_t* residual;
+    int64_t n;
+    int64_t rows_per_wave;
+    int ng;
+    int prologue;
+    float eps;
+};
+
+__device__ __forceinline__ float h2f(uint32_t bits16) { return __half2float(__ushort_as_half((uint16_t)bits16)); }
+__device__ __forceinline__ uint32_t f2h(float v) { return __half_as_ushort(__float2half_rn(v)); }
+
+// Sum over the block in a fixed order (every thread gets the same value).
+__device__ __forceinline__ float block_sum(float v, float* red) {
+    v = segment_sum<kWave>(v);  // the wave's total lands in its last lane
+    if ((threadIdx.x & (kWave - 1)) == kWave - 1) red[threadIdx.x / kWave] = v;
+    __syncthreads();
+    float t = red[0];
+#pragma unroll
+    for (int w = 1; w < kWavesPerBlock; ++w) t += red[w];
+    return t;
+}
+
+// x_eff of the whole row into LDS (all threads of the block take part).
+__device__ __forceinline__ void stage_prologue(const Args& a, uint16_t* s_x, float* red) {
+    const int tid = threadIdx.x;
+    const int chunks = a.ng * (kGroup / 8);
+    const WQ_GLOBAL u32x4* xs = gbl(reinterpret_cast<const u32x4*>(a.x));
+    const WQ_GLOBAL u32x4* bs = a.prologue == WQ_PROLOGUE_RMSNORM
+                                    ? gbl(reinterpret_cast<const u32x4*>(a.norm))
+                                    : gbl(reinterpret_cast<const u32x4*>(a.x)) + chunks;  // the up half
+    u32x4 xa[kChunksPerThread], xb[kChunksPerThread];
+#pragma unroll
+    for (int r = 0; r < kChunksPerThread; ++r) {
+        const int c = tid + r * kBlock;
+        if (c < chunks) {
+            xa[r] = xs[c];
+            xb[r] = bs[c];
+        }
+    }
+    float inv = 0.0f;
+    if (a.prologue == WQ_PROLOGUE_RMSNORM) {
+        float ss = 0.0f;
+#pragma unroll
+        for (int r = 0; r < kChunksPerThread; ++r) {
+            if (tid + r * kBlock >= chunks) continue;
+            const uint32_t w[4] = {xa[r].x, xa[r].y, xa[r].z, xa[r].w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float lo = h2f(w[i] & 0xFFFFu), hi = h2f(w[i] >> 16);
+                ss = fmaf(lo, lo, ss);
+                ss = fmaf(hi, hi, ss);
+            }
+        }
+        const float total = block_sum(ss, red);
+        inv = 1.0f / sqrtf(total / (float)(a.ng * kGroup) + a.eps);
+    }
+#pragma unroll
+    for (int r = 0; r < kChunksPerThread; ++r) {
+        const int c = tid + r * kBlock;
+        if (c >= chunks) continue;
+        const uint32_t wa[4] = {xa[r].x, xa[r].y, xa[r].z, xa[r].w};
+        const uint32_t wb[4] = {xb[r].x, xb[r].y, xb[r].z, xb[r].w};
+        uint32_t o[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            float v[2];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const float p = h2f(h ? wa[i] >> 16 : wa[i] & 0xFFFFu);
+                const float q = h2f(h ? wb[i] >> 16 : wb[i] & 0xFFFFu);
+                v[h] = a.prologue == WQ_PROLOGUE_RMSNORM ? (p * inv) * q : p / (1.0f + expf(-p)) * q;
+            }
+            o[i] = f2h(v[0]) | (f2h(v[1]) << 16);
+        }
+        reinterpret_cast<u32x4*>(s_x)[c] = u32x4{o[0], o[1], o[2], o[3]};
+    }
+    __syncthreads();
+}
+
+// load_x_lane with x_eff already in LDS.
+template <int LPR, int GPL>
+__device__ __forceinline__ void load_x_lane_lds(const uint16_t* s_x, int ng, int lane, half2v (&xr)[GPL][16]) {
+    const int sub = lane & (LPR - 1);
+#pragma unroll
+    for (int j = 0; j < GPL; ++j) {
+        const bool act = sub + LPR * j < ng;
+        const u32x4* src = reinterpret_cast<const u32x4*>(s_x + min(sub + LPR * j, ng - 1) * kGroup);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const u32x4 d = src[c];
+            xr[j][4 * c + 0] = as_h2(act ? (d.x & 0xFFFFu) | (d.z << 16) : 0u);
+            xr[j][4 * c + 1] = as_h2(act ? (d.x >> 16) | (d.z & 0xFFFF0000u) : 0u);
+            xr[j][4 * c + 2] = as_h2(act ? (d.y & 0xFFFFu) | (d.w << 16) : 0u);
+            xr[j][4 * c + 3] = as_h2(act ? (d.y >> 16) | (d.w & 0xFFFF0000u) : 0u);
+        }
+    }
+}
+
+// compute_step with the row sums staged as fp32 (the residual is added later).
+template <int LPR, int GPL>
+__device__ __forceinline__ void compute_step_f32(const StepBuf& b, const half2v (&xr)[GPL][16], int nrows,
+                                                 float* ylds, int yrel, int lane) {
+    using S = StepShape<LPR, GPL>;
+    const int slot = lane / LPR;
+    const int sub = lane & (LPR - 1);
+#pragma unroll
+    for (int u = 0; u < S::U; ++u) {
+        float acc = 0.0f;
+#pragma unroll
+        for (int j = 0; j < GPL; ++j) {
+            const float s = h2f(b.s[u * GPL + j]);
+            acc = fmaf(s, dot_group(b.w[u * GPL + j], xr[j]), acc);
+        }
+        const float tot = segment_sum<LPR>(acc);
+        const int rr = slot * S::U + u;
+        if (sub == LPR - 1 && rr < nrows) ylds[yrel + rr] = tot;
+    }
+}
+
+__device__ __forceinline__ void flush_y_residual(uint16_t* y, const uint16_t* residual, int64_t row0,
+                                                 const float* ylds, int count, int lane) {
+    wave_lds_sync();
+    WQ_GLOBAL uint16_t* dst = gbl(y) + row0;
+    if (residual) {
+        const WQ_GLOBAL uint16_t* res = gbl(residual) + row0;
+        for (int i = lane; i < count; i += kWave) dst[i] = (uint16_t)f2h(ylds[i] + h2f(res[i]));
+    } else {
+        for (int i = lane; i < count; i += kWave) dst[i] = (uint16_t)f2h(ylds[i]);
+    }
+    wave_lds_sync();
+}
+
+template <int LPR, int GPL>
+__global__ __launch_bounds__(kBlock) void fused_m1_kernel(const Args a) {
+    constexpr int R = StepShape<LPR, GPL>::ROWS;
+    extern __shared__ __align__(16) uint16_t s_x[];  // x_eff, K entries (prologues only)
+    __shared__ __align__(16) float s_y[kWavesPerBlock][kYRows];
+    __shared__ float s_red[kWavesPerBlock];
+    const int lane = threadIdx.x & (kWave - 1);
+
+    half2v xr[GPL][16];
+    if (a.prologue != WQ_PROLOGUE_NONE) {
+        stage_prologue(a, s_x, s_red);
+        load_x_lane_lds<LPR, GPL>(s_x, a.ng, lane, xr);
+    } else {
+        load_x_lane<LPR, GPL, GPL>(a.x, a.ng, lane, xr);
+    }
+
+    const int64_t wave = (int64_t)__builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerBlock + threadIdx.x / kWave);
+    const int64_t rb = wave * a.rows_per_wave;
+    if (rb >= a.n) return;
+    const int64_t re = min(a.n, rb + a.rows_per_wave);
+    const int64_t steps = (re - rb + R - 1) / R;
+    const LinearRsrc rs = make_rsrc(a.packed, a.scales, (uint32_t)(a.n * a.ng * 2));
+    float* ylds = s_y[threadIdx.x / kWave];
+
+    // As in gemv_m1_kernel: unconditional issues from two sites, so the wait
+    // counts stay exact; past the matrix the loads read zeros.
+    StepBuf b0, b1;
+    for (int64_t s = -2; s < steps; s += 2) {
+        const int64_t ra = rb + s * R;
+        if (s >= 0) compute_step_f32<LPR, GPL>(b0, xr, (int)min((int64_t)R, re - ra), ylds, (int)(s * R), lane);
+        issue_step<LPR, GPL>(b0, rs, ra + 2 * R, a.ng, lane);
+        const int64_t rbb = ra + R;
+        if (s + 1 >= 0 && s + 1 < steps)
+            compute_step_f32<LPR, GPL>(b1, xr, (int)min((int64_t)R, re - rbb), ylds, (int)((s + 1) * R), lane);
+        issue_step<LPR, GPL>(b1, rs, rbb + 2 * R, a.ng, lane);
+    }
+    flush_y_residual(a.y, a.residual, rb, ylds, (int)(re - rb), lane);
+}
+
+// (value, index) pairs: a larger value wins, then a smaller index; index -1
+// (nothing seen, or only NaN) loses to anything.
+__device__ __forceinline__ bool beats(float v2, int64_t i2, float v1, int64_t i1) {
+    if (i2 < 0) return false;
+    if (i1 < 0) return true;
+    return v2 > v1 || (v2 == v1 && i2 < i1);
+}
+
+__global__ __launch_bounds__(kArgThreads) void argmax_kernel(const uint16_t* y, int64_t n, int32_t* out) {
+    constexpr int kWaves = kArgThreads / kWave;
+    __shared__ float s_v[kWaves];
+    __shared__ int64_t s_i[kWaves];
+    const WQ_GLOBAL uint16_t* src = gbl(y);
+    float best = 0.0f;
+    int64_t bi = -1;
+    for (int64_t i = threadIdx.x; i < n; i += kArgThreads) {
+        const float v = h2f(src[i]);
+        if (v == v && (bi < 0 || v > best)) {
+            best = v;
+            bi = i;
+        }
+    }
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1) {
+        const float v2 = __shfl_xor(best, o);
+        const int64_t i2 = __shfl_xor(bi, o);
+        if (beats(v2, i2, best, bi)) {
+            best = v2;
+            bi = i2;
+        }
+    }
+    if ((threadIdx.x & (kWave - 1)) == 0) {
+        s_v[threadIdx.x / kWave] = best;
+        s_i[threadIdx.x / kWave] = bi;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float v = s_v[0];
+        int64_t i = s_i[0];
+        for (int w = 1; w < kWaves; ++w)
+            if (beats(s_v[w], s_i[w], v, i)) {
+                v = s_v[w];
+                i = s_i[w];
+            }
+        *out = (int32_t)i;
+    }
+}
+
+// ------------------------------------------------------------------- host
+
+template <int LPR, int GPL>
+hipError_t launch_fused(const wq_fused_linear& l, hipStream_t stream) {
+    constexpr int R = StepShape<LPR, GPL>::ROWS;
+    const int64_t ng = l.K / kGroup;
+    const int64_t steps = (l.N + R - 1) / R;
+    const int64_t steps_per_wave = std::min((steps + kTargetWaves - 1) / kTargetWaves, (int64_t)(kYRows / R));
+    Args a;
+    a.packed = reinterpret_cast<const u32x4*>(l.packed_w);
+    a.scales = l.scales;
+    a.x = l.x;
+    a.y = l.y;
+    a.norm = l.norm_weight;
+    a.residual = l.residual;
+    a.n = l.N;
+    a.rows_per_wave = steps_per_wave * R;
+    a.ng = (int)ng;
+    a.prologue = l.prologue;
+    a.eps = l.eps;
+    const int64_t waves = (l.N + a.rows_per_wave - 1) / a.rows_per_wave;
+    const int64_t blocks = (waves + kWavesPerBlock - 1) / kWavesPerBlock;
+    const size_t lds = l.prologue == WQ_PROLOGUE_NONE ? 0 : (size_t)l.K * 2;
+    hipLaunchKernelGGL((fused_m1_kernel<LPR, GPL>), dim3((unsigned)blocks), dim3(kBlock), lds, stream, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_one(const wq_fused_linear& l, hipStream_t stream) {
+    int lpr = 64, gpl = 1;
+    pick_shape((int)(l.K / kGroup), lpr, gpl);
+#define WQ_FUSED_CASE(L, G) \
+    if (lpr == L && gpl == G) return launch_fused<L, G>(l, stream);
+    WQ_FUSED_CASE(64, 1) WQ_FUSED_CASE(64, 2) WQ_FUSED_CASE(64, 3) WQ_FUSED_CASE(64, 4)
+    WQ_FUSED_CASE(64, 5) WQ_FUSED_CASE(64, 6) WQ_FUSED_CASE(64, 7) WQ_FUSED_CASE(64, 8)
+    WQ_FUSED_CASE(32, 1) WQ_FUSED_CASE(32, 3) WQ_FUSED_CASE(32, 5) WQ_FUSED_CASE(32, 7)
+    WQ_FUSED_CASE(16, 1) WQ_FUSED_CASE(16, 3) WQ_FUSED_CASE(16, 5) WQ_FUSED_CASE(16, 7)
+#undef WQ_FUSED_CASE
+    return hipErrorInvalidValue;  // pick_shape returns only the shapes above
+}
+
+wq_status err(wq_status st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+wq_status err(wq_status st, const char* fmt, ...) {
+    char msg[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(msg, sizeof(msg), fmt, ap);
+    va_end(ap);
+    return record_error(st, msg);
+}
+
+bool aligned(const void* p, uintptr_t a) { return reinterpret_cast<uintptr_t>(p) % a == 0; }
+
+struct Span {
+    uintptr_t lo, hi;
+};
+Span span(const void* p, uint64_t bytes) {
+    const uintptr_t lo = reinterpret_cast<uintptr_t>(p);
+    return Span{lo, lo + (uintptr_t)bytes};
+}
+bool overlaps(Span a, Span b) { return a.lo < a.hi && b.lo < b.hi && a.lo < b.hi && b.lo < a.hi; }
+
+// Sorted, merged union of spans, for "does s overlap any of them".
+struct SpanUnion {
+    std::vector<Span> v;
+    void build(std::vector<Span> in) {
+        std::sort(in.begin(), in.end(), [](const Span& p, const Span& q) { return p.lo < q.lo; });
+        for (const Span& s : in) {
+            if (s.lo >= s.hi) continue;
+            if (!v.empty() && s.lo <= v.back().hi) v.back().hi = std::max(v.back().hi, s.hi);
+            else v.push_back(s);
+        }
+    }
+    bool hits(Span s) const {
+        auto it = std::lower_bound(v.begin(), v.end(), s.hi, [](const Span& p, uintptr_t x) { return p.lo < x; });
+        return it != v.begin() && overlaps(*std::prev(it), s);
+    }
+};
+
+wq_status check_linear(const char* fn, int64_t i, const wq_fused_linear& l) {
+    if (!l.packed_w || !l.scales || !l.x || !l.y)
+        return err(WQ_ERR_INVALID_ARG, "%s: linear %lld: null pointer", fn, (long long)i);
+    if (l.prologue != WQ_PROLOGUE_NONE && l.prologue != WQ_PROLOGUE_RMSNORM && l.prologue != WQ_PROLOGUE_SILU_MUL)
+        return err(WQ_ERR_INVALID_ARG, "%s: linear %lld: unknown prologue %d", fn, (long long)i, (int)l.prologue);
+    if (l.prologue == WQ_PROLOGUE_RMSNORM) {
+        if (!l.norm_weight) return err(WQ_ERR_INVALID_ARG, "%s: linear %lld: null norm_weight", fn, (long long)i);
+        if (!std::isfinite(l.eps) || l.eps < 0.0f)
+            return err(WQ_ERR_INVALID_ARG, "%s: linear %lld: eps must be finite and >= 0", fn, (long long)i);
+    }
+    if (l.N <= 0 || l.K <= 0 || l.N > WQ_MAX_N)
+        return err(WQ_ERR_INVALID_ARG, "%s: linear %lld: N and K must be positive (N=%lld K=%lld)", fn, (long long)i,
+                   (long long)l.N, (long long)l.K);
+    if (l.K % kGroup != 0 || l.K > WQ_FUSED_MAX_K)
+        return err(WQ_ERR_UNSUPPORTED, "%s: linear %lld: K must be a multiple of 32 up to %lld (K=%lld)", fn,
+                   (long long)i, (long long)WQ_FUSED_MAX_K, (long long)l.K);
+    if (!fits_rsrc(l.N, l.K / kGroup))
+        return err(WQ_ERR_UNSUPPORTED, "%s: linear %lld: codes above 4 GiB", fn, (long long)i);
+    if (!aligned(l.packed_w, 16) || !aligned(l.x, 16) ||
+        (l.prologue == WQ_PROLOGUE_RMSNORM && !aligned(l.norm_weight, 16)))
+        return err(WQ_ERR_MISALIGNED, "%s: linear %lld: packed_w, x and norm_weight must be 16-byte aligned", fn,
+                   (long long)i);
+    if (!aligned(l.scales, 2) || !aligned(l.y, 2) || !aligned(l.residual, 2))
+        return err(WQ_ERR_MISALIGNED, "%s: linear %lld: scales, y and residual must be 2-byte aligned", fn,
+                   (long long)i);
+    const Span y = span(l.y, 2 * l.N);
+    const int64_t xk = l.prologue == WQ_PROLOGUE_SILU_MUL ? 2 * l.K : l.K;
+    if (overlaps(y, span(l.x, 2 * xk)))
+        return err(WQ_ERR_INVALID_ARG, "%s: linear %lld: y overlaps x", fn, (long long)i);
+    if (l.prologue == WQ_PROLOGUE_RMSNORM && overlaps(y, span(l.norm_weight, 2 * l.K)))
+        return err(WQ_ERR_INVALID_ARG, "%s: linear %lld: y overlaps norm_weight", fn, (long long)i);
+    if (l.residual && l.residual != l.y && overlaps(y, span(l.residual, 2 * l.N)))
+        return err(WQ_ERR_INVALID_ARG, "%s: linear %lld: residual overlaps y without being y", fn, (long long)i);
+    return WQ_OK;
+}
+
+}  // namespace
+}  // namespace fused
+}  // namespace wq
+
+using namespace wq::fused;
+
+extern "C" wq_status wq_fused_linears(const wq_fused_linear* linears, int64_t count, int32_t* argmax,
+                                      int64_t group, void* stream) {
+    static const char* fn = "wq_fused_linears";
+    if (!linears) return err(WQ_ERR_INVALID_ARG, "%s: null descriptor array", fn);
+    if (count <= 0 || count > WQ_MAX_LINEARS)
+        return err(WQ_ERR_INVALID_ARG, "%s: count must be in [1, %lld] (count=%lld)", fn, (long long)WQ_MAX_LINEARS,
+                   (long long)count);
+    if (group != 32) return err(WQ_ERR_UNSUPPORTED, "%s: only group=32 is supported (got %lld)", fn, (long long)group);
+    if (argmax && !aligned(argmax, 4)) return err(WQ_ERR_MISALIGNED, "%s: argmax must be 4-byte aligned", fn);
+    std::vector<wq_fused_linear> lin(linears, linears + count);
+    std::vector<Span> weights, all;
+    for (int64_t i = 0; i < count; ++i) {
+        const wq_status st = check_linear(fn, i, lin[i]);
+        if (st != WQ_OK) return st;
+        const wq_fused_linear& l = lin[i];
+        weights.push_back(span(l.packed_w, l.N * l.K / 2));
+        weights.push_back(span(l.scales, l.N * (l.K / kGroup) * 2));
+    }
+    SpanUnion wu;
+    wu.build(weights);
+    for (int64_t i = 0; i < count; ++i) {
+        const wq_fused_linear& l = lin[i];
+        if (wu.hits(span(l.y, 2 * l.N)))
+            return err(WQ_ERR_INVALID_ARG, "%s: y of linear %lld overlaps packed_w or scales of a linear", fn,
+                       (long long)i);
+        if (argmax) {
+            const int64_t xk = l.prologue == WQ_PROLOGUE_SILU_MUL ? 2 * l.K : l.K;
+            all.push_back(span(l.x, 2 * xk));
+            all.push_back(span(l.y, 2 * l.N));
+            if (l.prologue == WQ_PROLOGUE_RMSNORM) all.push_back(span(l.norm_weight, 2 * l.K));
+            if (l.residual) all.push_back(span(l.residual, 2 * l.N));
+        }
+    }
+    if (argmax) {
+        SpanUnion au;
+        all.insert(all.end(), weights.begin(), weights.end());
+        au.build(all);
+        if (au.hits(span(argmax, 4))) return err(WQ_ERR_INVALID_ARG, "%s: argmax overlaps an array of the chain", fn);
+    }
+    (void)hipGetLastError();
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    for (int64_t i = 0; i < count; ++i) {
+        const hipError_t e = launch_one(lin[i], s);
+        if (e != hipSuccess)
+            return err(WQ_ERR_HIP, "%s: linear %lld: HIP error %d (%s)", fn, (long long)i, (int)e, hipGetErrorString(e));
+    }
+    if (argmax) {
+        const wq_fused_linear& last = lin[count - 1];
+        hipLaunchKernelGGL(argmax_kernel, dim3(1), dim3(kArgThreads), 0, s, last.y, last.N, argmax);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return err(WQ_ERR_HIP, "%s: argmax: HIP error %d (%s)", fn, (int)e, hipGetErrorString(e));
+    }
+    return WQ_OK;
+}

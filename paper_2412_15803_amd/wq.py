@@ -1,4 +1,5 @@
-"""Thin ctypes binding of the C ABI in include/wq.h and include/wq_attention.h.
+"""Thin ctypes binding of the C ABI in include/wq.h, include/wq_attention.h and
+include/wq_fused.h.
 
 Only argument marshalling happens here: torch tensors are turned into device
 pointers and sizes, the current HIP stream is passed through, and non-OK
@@ -24,7 +25,12 @@ GROUP = 32
 
 # Every function declared in the headers under include/.
 EXPORTED = ("wq_status_string", "wq_last_error_message", "wq_version", "wq_pack", "wq_gemv",
-            "wq_decode_linears", "wq_paged_attention_workspace_size", "wq_paged_attention")
+            "wq_decode_linears", "wq_paged_attention_workspace_size", "wq_paged_attention",
+            "wq_fused_linears")
+
+PROLOGUE_NONE = 0
+PROLOGUE_RMSNORM = 1
+PROLOGUE_SILU_MUL = 2
 
 
 class WqLinear(ctypes.Structure):
@@ -35,6 +41,21 @@ class WqLinear(ctypes.Structure):
         ("y", ctypes.c_void_p),
         ("N", ctypes.c_int64),
         ("K", ctypes.c_int64),
+    ]
+
+
+class WqFusedLinear(ctypes.Structure):
+    _fields_ = [
+        ("packed_w", ctypes.c_void_p),
+        ("scales", ctypes.c_void_p),
+        ("x", ctypes.c_void_p),
+        ("y", ctypes.c_void_p),
+        ("norm_weight", ctypes.c_void_p),
+        ("residual", ctypes.c_void_p),
+        ("N", ctypes.c_int64),
+        ("K", ctypes.c_int64),
+        ("prologue", ctypes.c_int32),
+        ("eps", ctypes.c_float),
     ]
 
 
@@ -74,6 +95,8 @@ def lib() -> ctypes.CDLL:
     L.wq_paged_attention.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, i64, i64, i64,
                                      ctypes.c_float, vp, ctypes.c_size_t, vp]
     L.wq_paged_attention.restype = ctypes.c_int
+    L.wq_fused_linears.argtypes = [ctypes.POINTER(WqFusedLinear), i64, vp, i64, vp]
+    L.wq_fused_linears.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -233,3 +256,46 @@ def paged_attention(q, k_cache, v_cache, block_table, seq_lens, out, scale: floa
     _check(lib().wq_paged_attention(pq, pk, pv, pt, pl, po, num_seqs, hq, hkv, d, page, num_pages,
                                     max_pages, max_seq_len, float(scale), pw, nw,
                                     _stream(stream, q.device)))
+
+
+# ------------------------------------------------------- fused decode chain
+
+def make_fused_array(linears, group: int = GROUP):
+    """Marshal dicts with keys packed_w, scales, x, y (tensors) and optional
+    prologue (PROLOGUE_*), norm_weight, eps, residual into a ctypes
+    wq_fused_linear array.  x is [K] ([2K] for PROLOGUE_SILU_MUL), y and
+    residual [N], norm_weight [K]; 1-D or [1, n] tensors are accepted."""
+    arr = (WqFusedLinear * len(linears))()
+    for i, d in enumerate(linears):
+        packed_w, scales, x, y = d["packed_w"], d["scales"], d["x"], d["y"]
+        pro = int(d.get("prologue", PROLOGUE_NONE))
+        n = packed_w.shape[0]
+        k = packed_w.shape[1] * 8
+        xk = 2 * k if pro == PROLOGUE_SILU_MUL else k
+        arr[i].packed_w = _dev_tensor(packed_w, f"linears[{i}].packed_w", _word_dtypes(), (n, k // 8)).value
+        arr[i].scales = _dev_tensor(scales, f"linears[{i}].scales", _half_dtypes(), (n, k // group)).value
+        arr[i].x = _dev_tensor(x.reshape(-1), f"linears[{i}].x", _half_dtypes(), (xk,)).value
+        arr[i].y = _dev_tensor(y.reshape(-1), f"linears[{i}].y", _half_dtypes(), (n,)).value
+        norm = d.get("norm_weight")
+        arr[i].norm_weight = _dev_tensor(norm, f"linears[{i}].norm_weight", _half_dtypes(), (k,)).value \
+            if norm is not None else None
+        res = d.get("residual")
+        arr[i].residual = _dev_tensor(res.reshape(-1), f"linears[{i}].residual", _half_dtypes(), (n,)).value \
+            if res is not None else None
+        arr[i].N = n
+        arr[i].K = k
+        arr[i].prologue = pro
+        arr[i].eps = float(d.get("eps", 0.0))
+    return arr
+
+
+def wq_fused_linears(linears, argmax=None, group: int = GROUP, stream=None, _array=None) -> None:
+    """Run a chain of fused linears in order (see make_fused_array); when
+    `argmax` (a device int32 tensor of one element) is given, the index of
+    the largest element of the last linear's y is written to it."""
+    import torch
+
+    arr = _array if _array is not None else make_fused_array(linears, group)
+    device = linears[0]["x"].device
+    pa = _dev_tensor(argmax.reshape(-1), "argmax", (torch.int32,), (1,)) if argmax is not None else None
+    _check(lib().wq_fused_linears(arr, len(arr), pa, group, _stream(stream, device)))

@@ -241,3 +241,64 @@ def test_attention_workspace_size(L):
     # the call accepts exactly the reported size and no less
     n = workspace_bytes(L, 1, 24, 8, 128, 4096)[1]
     assert attention(L, ws_bytes=n - 1) == 1
+
+
+# ------------------------------------------------------- fused linears
+
+def _fused(n_lin, override=None):
+    from paper_2412_15803_amd.wq import WqFusedLinear
+
+    arr = (WqFusedLinear * n_lin)()
+    for i in range(n_lin):
+        base = 0x10000000 * (i + 1)
+        arr[i].packed_w, arr[i].scales = base, base + 0x1000000
+        arr[i].x, arr[i].y = base + 0x2000000, base + 0x3000000
+        arr[i].norm_weight, arr[i].residual = base + 0x4000000, None
+        arr[i].N, arr[i].K, arr[i].prologue, arr[i].eps = 64, 64, 1, 1e-5
+    for (i, field), val in (override or {}).items():
+        setattr(arr[i], field, val)
+    return arr
+
+
+@pytest.mark.parametrize(
+    "override,status,needle",
+    [
+        ({(0, "x"): None}, 1, "null"),
+        ({(1, "norm_weight"): None}, 1, "norm_weight"),
+        ({(1, "prologue"): 3}, 1, "prologue"),
+        ({(0, "eps"): -1.0}, 1, "eps"),
+        ({(0, "eps"): float("inf")}, 1, "eps"),
+        ({(0, "N"): 0}, 1, "positive"),
+        ({(0, "K"): 48}, 2, "multiple of 32"),
+        ({(0, "K"): 16416}, 2, "multiple of 32"),
+        ({(0, "x"): 0x12000008}, 3, "16-byte"),
+        ({(0, "norm_weight"): 0x14000002}, 3, "16-byte"),
+        ({(0, "y"): 0x13000001}, 3, "2-byte"),
+        ({(0, "residual"): 0x15000001}, 3, "2-byte"),
+        ({(0, "y"): 0x12000000 + 64}, 1, "y overlaps x"),
+        ({(0, "y"): 0x14000000 + 16}, 1, "norm_weight"),
+        ({(0, "residual"): 0x13000000 + 2}, 1, "residual overlaps y"),
+        ({(1, "y"): 0x10000000 + 64}, 1, "overlaps packed_w or scales"),
+        # SILU_MUL reads 2K entries of x: y right after the first K overlaps
+        ({(0, "prologue"): 2, (0, "y"): 0x12000000 + 128}, 1, "y overlaps x"),
+    ],
+)
+def test_fused_rejects(L, override, status, needle):
+    arr = _fused(2, override)
+    st = L.wq_fused_linears(arr, 2, None, 32, None)
+    assert st == status, L.wq_last_error_message()
+    assert needle in L.wq_last_error_message().decode()
+
+
+def test_fused_rejects_call_level(L):
+    arr = _fused(2)
+    assert L.wq_fused_linears(None, 2, None, 32, None) == 1
+    assert L.wq_fused_linears(arr, 0, None, 32, None) == 1
+    assert L.wq_fused_linears(arr, 2, None, 64, None) == 2
+    assert L.wq_fused_linears(arr, 2, vp(0x30000002), 32, None) == 3
+    # argmax inside an array of the chain (the second linear's y)
+    assert L.wq_fused_linears(arr, 2, vp(0x20000000 + 0x3000000 + 8), 32, None) == 1
+    assert "argmax overlaps" in L.wq_last_error_message().decode()
+    # residual equal to y (an in-place add) is accepted by validation
+    ok = _fused(1, {(0, "residual"): 0x13000000})
+    assert ok[0].residual == ok[0].y
