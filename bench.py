@@ -322,6 +322,120 @@ def time_attention_rotated(hq, hkv, lens, page, seed, device, calls=256, reps=5,
     return round(ms * 1e3, 2), round(per / (ms * 1e-3) / 1e9, 1), per
 
 
+def time_dependent_step(lins, device, seed, ctx=4096, steps=20, reps=3):
+    """The 3B-class step as one token's dependent chain (batch 1), reusing the
+    step's packed weights: per layer RMSNorm -> qkv, attention of the 24
+    query heads (q = the first 3072 qkv outputs) over a paged cache of `ctx`
+    tokens, O + residual, RMSNorm -> gate_up, SiLU-mul -> down + residual;
+    then RMSNorm -> lm_head and argmax.  With ctx = 0 the attention is left
+    out (O reads the first 3072 qkv outputs) and the 113 linears run as one
+    wq_fused_linears call.  The step is replayed from one HIP graph, its
+    residual stream reset at the start of every replay; every replay must
+    reproduce the eager step's logits and token.
+
+    Returns {us per token, tokens/s, GB/s and fraction of the HBM peak over
+    the weights (and cached keys and values) read once per token}."""
+    import torch
+
+    from paper_2412_15803_amd import attn_workloads as aw
+    from paper_2412_15803_amd import workloads as wl
+    from paper_2412_15803_amd import wq
+
+    hid, layers = 3072, wl.LLAMA3B_LAYERS
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed + 77)
+
+    def vec(n, lo=None):
+        t = torch.rand(n, generator=gen, device=device) + 0.5 if lo else torch.randn(n, generator=gen, device=device)
+        return t.to(torch.float16)
+
+    h0, h = vec(hid), torch.empty(hid, dtype=torch.float16, device=device)
+    qkv = torch.empty(5120, dtype=torch.float16, device=device)
+    attn = torch.empty(hid, dtype=torch.float16, device=device)
+    gu = torch.empty(16384, dtype=torch.float16, device=device)
+    logits = torch.empty(128256, dtype=torch.float16, device=device)
+    token = torch.empty(1, dtype=torch.int32, device=device)
+    norm1 = [vec(hid, True) for _ in range(layers)]
+    norm2 = [vec(hid, True) for _ in range(layers)]
+    norm_f = vec(hid, True)
+    eps = 1e-5
+
+    def lin(i, x, y, **kw):
+        p, sc = lins[i][0], lins[i][1]
+        return dict(packed_w=p, scales=sc, x=x, y=y, eps=eps, **kw)
+
+    R, S = wq.PROLOGUE_RMSNORM, wq.PROLOGUE_SILU_MUL
+    per_layer = []
+    for l in range(layers):
+        b = 4 * l
+        qkv_lin = lin(b, h, qkv, prologue=R, norm_weight=norm1[l])
+        rest = [lin(b + 1, attn if ctx else qkv[:hid], h, residual=h),
+                lin(b + 2, h, gu, prologue=R, norm_weight=norm2[l]),
+                lin(b + 3, gu, h, prologue=S, residual=h)]
+        per_layer.append((qkv_lin, rest))
+    head = lin(4 * layers, h, logits, prologue=R, norm_weight=norm_f)
+
+    step_bytes = sum(wl.ideal_bytes(p.shape[0], p.shape[1] * 8, 1) for p, _, _, _ in lins)
+    if ctx:
+        need = aw.pages_needed((ctx,), 16)
+        k_all, v_all = aw.kv_cache_device(seed + 78, layers * need, 8, 16, aw.HEAD_DIM, device=device)
+        caches = [(k_all[i * need:(i + 1) * need], v_all[i * need:(i + 1) * need]) for i in range(layers)]
+        table_np, _ = aw.block_table_host(seed + 79, (ctx,), 16)
+        table = torch.from_numpy(table_np).to(device)
+        lens = torch.tensor([ctx], dtype=torch.int32, device=device)
+        ws = wq.paged_workspace(qkv[:hid].view(1, 24, aw.HEAD_DIM), ctx, 8)
+        scale = aw.default_scale(aw.HEAD_DIM)
+        arrays = [(wq.make_fused_array([a]), wq.make_fused_array(r)) for a, r in per_layer]
+        head_arr = wq.make_fused_array([head])
+        step_bytes += layers * aw.attention_bytes((ctx,), 24, 8, aw.HEAD_DIM, 16)
+
+        def step():
+            h.copy_(h0)
+            for l in range(layers):
+                wq.wq_fused_linears([per_layer[l][0]], _array=arrays[l][0])
+                k, v = caches[l]
+                wq.paged_attention(qkv[:hid].view(1, 24, aw.HEAD_DIM), k, v, table, lens,
+                                   attn.view(1, 24, aw.HEAD_DIM), scale, ctx, workspace=ws)
+                wq.wq_fused_linears(per_layer[l][1], _array=arrays[l][1])
+            wq.wq_fused_linears([head], argmax=token, _array=head_arr)
+    else:
+        chain = [d for a, r in per_layer for d in [a] + r] + [head]
+        chain_arr = wq.make_fused_array(chain)
+
+        def step():
+            h.copy_(h0)
+            wq.wq_fused_linears(chain, argmax=token, _array=chain_arr)
+
+    side = torch.cuda.Stream(device)
+    side.wait_stream(torch.cuda.current_stream(device))
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream(device).wait_stream(side)
+    torch.cuda.synchronize()
+    ref_logits, ref_token = logits.clone(), int(token.item())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    times = []
+    for _ in range(reps):
+        a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(steps):
+            graph.replay()
+        e.record()
+        torch.cuda.synchronize()
+        times.append(a.elapsed_time(e) / steps)
+        if int(token.item()) != ref_token or not torch.equal(logits, ref_logits):
+            raise RuntimeError("graph replay of the dependent step differs from the eager step")
+    ms = sorted(times)[len(times) // 2]
+    del graph
+    torch.cuda.empty_cache()
+    gbs = step_bytes / (ms * 1e-3) / 1e9
+    return {"us_per_token": round(ms * 1e3, 1), "tokens_per_s": round(1e3 / ms, 1), "GB_s": round(gbs, 1),
+            "frac": round(gbs / HBM_PEAK_GBS, 4), "bytes_per_token": step_bytes, "token": ref_token,
+            "finite_logits": bool(torch.isfinite(ref_logits).all().item())}
+
+
 # Counter summaries of the split kernel, by ATTN_CONFIGS index.
 ATTN_PROFILES = {0: "paged_attention_3b_ctx4096.md", 1: "paged_attention_3b_ctx32768.md"}
 ATTN_SOURCES = ("wq_attention.hip", "wq_device.h")
@@ -475,6 +589,16 @@ def main():
                   f"{step_bytes / 1e6:.2f} MB algorithmic per launch)",
     }
 
+    dependent = None
+    if not args.no_configs:
+        log("timing the dependent decode step (fused linears and paged attention)")
+        dependent = {
+            "method": "one token's dependent layer chain (batch 1) with the step's weights, replayed from a HIP graph",
+            "linears only (113 fused linears, one wq_fused_linears call)": time_dependent_step(lins, device, args.seed,
+                                                                                              ctx=0),
+            "with attention over 4096 cached tokens per layer": time_dependent_step(lins, device, args.seed, ctx=4096),
+        }
+
     configs = None
     if not args.no_configs:
         log("timing the per-shape figures (single linears, small batches, 8B-class step)")
@@ -511,6 +635,7 @@ def main():
         },
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "dependent_decode_step": dependent,
         "per_config": configs,
     }
     print(json.dumps(out), flush=True)

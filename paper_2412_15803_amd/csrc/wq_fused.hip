@@ -12,9 +12,8 @@
 //     per element; each wave then stages its lanes' x_eff from LDS;
 //   * epilogue: row sums are staged in LDS as fp32, and the residual is added
 //     when y is written, so y is rounded once.
-// argmax_kernel: one 1024-thread workgroup scans the logits (each thread in
-// increasing index order, strict comparison) and reduces (value, index)
-// pairs with the smaller index winning ties.
+// argmax_kernel: one 1024-thread workgroup loads all logits in one round trip
+// and reduces (value, index) pairs, the smaller index winning ties.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 #include <math.h>
@@ -59,6 +58,14 @@ struct Args {
 
 __device__ __forceinline__ float h2f(uint32_t bits16) { return __half2float(__ushort_as_half((uint16_t)bits16)); }
 __device__ __forceinline__ uint32_t f2h(float v) { return __half_as_ushort(__float2half_rn(v)); }
+
+// silu(a) = a / (1 + e^-a) with the hardware exp2 and reciprocal (about one
+// ulp each): every block evaluates it for the whole row, and its fp32 error
+// stays far below the fp16 rounding that follows.  Large negative a gives
+// exp2 = inf and a * 0 = -0; large positive a gives exactly a.
+__device__ __forceinline__ float silu(float a) {
+    return a * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(a * -1.4426950408889634f));
+}
 
 // Sum over the block in a fixed order (every thread gets the same value).
 __device__ __forceinline__ float block_sum(float v, float* red) {
@@ -119,7 +126,7 @@ __device__ __forceinline__ void stage_prologue(const Args& a, uint16_t* s_x, flo
             for (int h = 0; h < 2; ++h) {
                 const float p = h2f(h ? wa[i] >> 16 : wa[i] & 0xFFFFu);
                 const float q = h2f(h ? wb[i] >> 16 : wb[i] & 0xFFFFu);
-                v[h] = a.prologue == WQ_PROLOGUE_RMSNORM ? (p * inv) * q : p / (1.0f + expf(-p)) * q;
+                v[h] = a.prologue == WQ_PROLOGUE_RMSNORM ? (p * inv) * q : silu(p) * q;
             }
             o[i] = f2h(v[0]) | (f2h(v[1]) << 16);
         }
@@ -228,18 +235,50 @@ __device__ __forceinline__ bool beats(float v2, int64_t i2, float v1, int64_t i1
     return v2 > v1 || (v2 == v1 && i2 < i1);
 }
 
+// Candidates of one thread: the scalar head before the first 16-byte
+// boundary, then 16-byte vectors (8 logits) issued kArgVec at a time so that
+// the whole vector of logits is in flight at once, then the scalar tail.
+constexpr int kArgVec = 16;
+
+__device__ __forceinline__ void take(float v, int64_t i, float& best, int64_t& bi) {
+    if (v == v && beats(v, i, best, bi)) {
+        best = v;
+        bi = i;
+    }
+}
+
 __global__ __launch_bounds__(kArgThreads) void argmax_kernel(const uint16_t* y, int64_t n, int32_t* out) {
     constexpr int kWaves = kArgThreads / kWave;
     __shared__ float s_v[kWaves];
     __shared__ int64_t s_i[kWaves];
+    const int tid = threadIdx.x;
     const WQ_GLOBAL uint16_t* src = gbl(y);
     float best = 0.0f;
     int64_t bi = -1;
-    for (int64_t i = threadIdx.x; i < n; i += kArgThreads) {
-        const float v = h2f(src[i]);
-        if (v == v && (bi < 0 || v > best)) {
-            best = v;
-            bi = i;
+    const int64_t head = min(n, (int64_t)((16 - (reinterpret_cast<uintptr_t>(y) & 15)) & 15) / 2);
+    const int64_t nv = (n - head) / 8;
+    const int64_t tail0 = head + nv * 8;
+    if (tid < head) take(h2f(src[tid]), tid, best, bi);
+    if (tail0 + tid < n) take(h2f(src[tail0 + tid]), tail0 + tid, best, bi);
+    const WQ_GLOBAL u32x4* vec = reinterpret_cast<const WQ_GLOBAL u32x4*>(src + head);
+    for (int64_t v0 = tid; v0 < nv; v0 += (int64_t)kArgThreads * kArgVec) {
+        u32x4 d[kArgVec];
+#pragma unroll
+        for (int u = 0; u < kArgVec; ++u) {
+            const int64_t v = v0 + (int64_t)u * kArgThreads;
+            if (v < nv) d[u] = vec[v];
+        }
+#pragma unroll
+        for (int u = 0; u < kArgVec; ++u) {
+            const int64_t v = v0 + (int64_t)u * kArgThreads;
+            if (v >= nv) continue;
+            const uint32_t w[4] = {d[u].x, d[u].y, d[u].z, d[u].w};
+            const int64_t e0 = head + 8 * v;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                take(h2f(w[e] & 0xFFFFu), e0 + 2 * e, best, bi);
+                take(h2f(w[e] >> 16), e0 + 2 * e + 1, best, bi);
+            }
         }
     }
 #pragma unroll
@@ -251,12 +290,12 @@ __global__ __launch_bounds__(kArgThreads) void argmax_kernel(const uint16_t* y, 
             bi = i2;
         }
     }
-    if ((threadIdx.x & (kWave - 1)) == 0) {
-        s_v[threadIdx.x / kWave] = best;
-        s_i[threadIdx.x / kWave] = bi;
+    if ((tid & (kWave - 1)) == 0) {
+        s_v[tid / kWave] = best;
+        s_i[tid / kWave] = bi;
     }
     __syncthreads();
-    if (threadIdx.x == 0) {
+    if (tid == 0) {
         float v = s_v[0];
         int64_t i = s_i[0];
         for (int w = 1; w < kWaves; ++w)

@@ -261,3 +261,63 @@ def test_fused_chain_equals_separate_calls():
     # and the first linear of the chain against the oracle
     ref, bound = oracle_linear(descs[0], h, None)
     assert fo.fused_within_tolerance(chain[0], ref, bound).all()
+
+
+def _argmax_through_residual(logits, offset):
+    """A linear with x = 0 and the logits as its residual returns exactly the
+    logits (0 + r, rounded once); its y starts `offset` elements into a
+    buffer, so the argmax kernel also sees unaligned vectors."""
+    import torch
+
+    from paper_2412_15803_amd import wq
+
+    require_gpu()
+    n = logits.shape[0]
+    packed, scales = random_linear(5 + n, n, 32)
+    x = torch.zeros(32, dtype=torch.float16, device="cuda:0")
+    buf = torch.full((n + offset,), float("nan"), dtype=torch.float16, device="cuda:0")
+    y = buf[offset:]
+    am = torch.full((1,), -7, dtype=torch.int32, device="cuda:0")
+    lin = {"packed_w": to_dev(packed), "scales": to_dev(scales).view(torch.float16), "x": x, "y": y,
+           "residual": to_dev(logits).view(torch.float16)}
+    wq.wq_fused_linears([lin], argmax=am)
+    torch.cuda.synchronize()
+    got_y = y.cpu().numpy()
+    assert np.array_equal(got_y.view(np.uint16), logits.view(np.uint16)) or \
+        np.array_equal(np.isnan(got_y), np.isnan(logits)), "residual pass-through changed the logits"
+    return int(am.cpu().item())
+
+
+def _first_max_ignoring_nan(v):
+    ok = ~np.isnan(v.astype(np.float32))
+    if not ok.any():
+        return -1
+    m = v[ok].max()
+    return int(np.flatnonzero(ok & (v == m))[0])
+
+
+@pytest.mark.parametrize("n", [1, 7, 8, 9, 17, 33, 1000, 16384 + 3, 128256])
+@pytest.mark.parametrize("offset", [0, 1, 5])
+def test_fused_argmax_edge_cases(n, offset):
+    announce(f"argmax n={n} offset={offset}")
+    rng = np.random.default_rng(n + offset)
+    base = _h(rng.standard_normal(n))
+    cases = [base]
+    tie = base.copy()
+    top = np.float16(9.0)
+    idx = sorted(set(int(i) for i in rng.integers(0, n, 3)))
+    tie[idx] = top                                   # equal maxima: the first must win
+    cases.append(tie)
+    neg = np.full(n, -np.inf, dtype=np.float16)      # all -inf: index 0
+    cases.append(neg)
+    if n > 2:
+        with_nan = base.copy()
+        with_nan[rng.integers(0, n, max(1, n // 4))] = np.nan
+        with_nan[0] = np.nan
+        cases.append(with_nan)
+    cases.append(np.full(n, np.nan, dtype=np.float16))   # nothing to choose: -1
+    for c in cases:
+        got = _argmax_through_residual(c, offset)
+        assert got == _first_max_ignoring_nan(c), (n, offset, got)
+        if not np.isnan(c.astype(np.float32)).any():
+            assert got == fo.argmax_first(c)
