@@ -48,6 +48,10 @@ def parse_args():
                     help="with --attention-only: time only this entry of ATTN_CONFIGS")
     ap.add_argument("--attention-eager", action="store_true",
                     help="with --attention-only: launch every call from the host (no HIP graph)")
+    ap.add_argument("--dependent-only", action="store_true",
+                    help="time only the dependent decode step (for profiling the fused kernels)")
+    ap.add_argument("--dependent-ctx", type=int, default=0,
+                    help="with --dependent-only: cached tokens per layer for attention (0: linears only)")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the per-shape figures (single linears, small batches, 8B-class step)")
     return ap.parse_args()
@@ -562,6 +566,13 @@ def main():
 
     log("building the 3B-class decode step (113 linears) on the device")
     plan, lins, step_bytes = build_step(args.seed, device)
+    if args.dependent_only:
+        if args.copy_probe_mib:
+            copy_probe(args.copy_probe_mib, device)
+        log(f"timing the dependent decode step ({args.dependent_ctx} cached tokens per layer)")
+        res = time_dependent_step(lins, device, args.seed, ctx=args.dependent_ctx, steps=args.steps, reps=3)
+        print(json.dumps({"dependent_decode_step": res}), flush=True)
+        return
     arr = wq.make_linear_array(lins, 1)
 
     if args.copy_probe_mib:

@@ -229,63 +229,91 @@ __global__ __launch_bounds__(kBlock) void fused_m1_kernel(const Args a) {
 
 // (value, index) pairs: a larger value wins, then a smaller index; index -1
 // (nothing seen, or only NaN) loses to anything.
-__device__ __forceinline__ bool beats(float v2, int64_t i2, float v1, int64_t i1) {
+__device__ __forceinline__ bool beats32(float v2, int i2, float v1, int i1) {
     if (i2 < 0) return false;
     if (i1 < 0) return true;
     return v2 > v1 || (v2 == v1 && i2 < i1);
 }
 
-// Candidates of one thread: the scalar head before the first 16-byte
-// boundary, then 16-byte vectors (8 logits) issued kArgVec at a time so that
-// the whole vector of logits is in flight at once, then the scalar tail.
+// Logits per thread: the scalar head before the first 16-byte boundary and
+// the scalar tail, plus up to kArgVec 16-byte vectors (8 logits each), all
+// loaded in one round trip.  A thread first takes the maximum of its vectors
+// (fmaxf ignores NaN), then the first element equal to it, scanning vectors
+// in increasing index order; the block then reduces the (value, index)
+// pairs.  NaN never wins; -1 when every logit is NaN.
 constexpr int kArgVec = 16;
 
-__device__ __forceinline__ void take(float v, int64_t i, float& best, int64_t& bi) {
-    if (v == v && beats(v, i, best, bi)) {
-        best = v;
-        bi = i;
-    }
-}
-
-__global__ __launch_bounds__(kArgThreads) void argmax_kernel(const uint16_t* y, int64_t n, int32_t* out) {
+__global__ __launch_bounds__(kArgThreads) void argmax_kernel(const uint16_t* y, int n, int32_t* out) {
     constexpr int kWaves = kArgThreads / kWave;
     __shared__ float s_v[kWaves];
-    __shared__ int64_t s_i[kWaves];
+    __shared__ int s_i[kWaves];
     const int tid = threadIdx.x;
     const WQ_GLOBAL uint16_t* src = gbl(y);
+    const int head = min(n, (int)(((16 - (reinterpret_cast<uintptr_t>(y) & 15)) & 15) / 2));
+    const int nv = (n - head) / 8;
+    const int tail0 = head + nv * 8;
     float best = 0.0f;
-    int64_t bi = -1;
-    const int64_t head = min(n, (int64_t)((16 - (reinterpret_cast<uintptr_t>(y) & 15)) & 15) / 2);
-    const int64_t nv = (n - head) / 8;
-    const int64_t tail0 = head + nv * 8;
-    if (tid < head) take(h2f(src[tid]), tid, best, bi);
-    if (tail0 + tid < n) take(h2f(src[tail0 + tid]), tail0 + tid, best, bi);
-    const WQ_GLOBAL u32x4* vec = reinterpret_cast<const WQ_GLOBAL u32x4*>(src + head);
-    for (int64_t v0 = tid; v0 < nv; v0 += (int64_t)kArgThreads * kArgVec) {
+    int bi = -1;
+    for (int v0 = tid; v0 < nv; v0 += kArgThreads * kArgVec) {
         u32x4 d[kArgVec];
+        const WQ_GLOBAL u32x4* vec = reinterpret_cast<const WQ_GLOBAL u32x4*>(src + head);
 #pragma unroll
         for (int u = 0; u < kArgVec; ++u) {
-            const int64_t v = v0 + (int64_t)u * kArgThreads;
-            if (v < nv) d[u] = vec[v];
+            const int v = v0 + u * kArgThreads;
+            d[u] = v < nv ? vec[v] : u32x4{0x7E007E00u, 0x7E007E00u, 0x7E007E00u, 0x7E007E00u};  // NaN
         }
+        float vmax[kArgVec];
+        float m = __builtin_nanf("");
 #pragma unroll
         for (int u = 0; u < kArgVec; ++u) {
-            const int64_t v = v0 + (int64_t)u * kArgThreads;
-            if (v >= nv) continue;
             const uint32_t w[4] = {d[u].x, d[u].y, d[u].z, d[u].w};
-            const int64_t e0 = head + 8 * v;
+            float t = __builtin_nanf("");   // stays NaN only for a vector of NaN
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                take(h2f(w[e] & 0xFFFFu), e0 + 2 * e, best, bi);
-                take(h2f(w[e] >> 16), e0 + 2 * e + 1, best, bi);
+            for (int e = 0; e < 4; ++e) t = fmaxf(t, fmaxf(h2f(w[e] & 0xFFFFu), h2f(w[e] >> 16)));
+            vmax[u] = t;
+            m = fmaxf(m, t);
+        }
+        int found = -1;   // the first vector holding the maximum (none if all NaN)
+#pragma unroll
+        for (int u = kArgVec - 1; u >= 0; --u)
+            if (vmax[u] == m) found = u;
+        if (found >= 0) {
+            u32x4 dv = d[0];
+#pragma unroll
+            for (int u = 1; u < kArgVec; ++u)
+                if (u == found) dv = d[u];
+            const uint32_t w[8] = {dv.x & 0xFFFFu, dv.x >> 16, dv.y & 0xFFFFu, dv.y >> 16,
+                                   dv.z & 0xFFFFu, dv.z >> 16, dv.w & 0xFFFFu, dv.w >> 16};
+            int e0 = -1;
+#pragma unroll
+            for (int e = 7; e >= 0; --e)
+                if (h2f(w[e]) == m) e0 = e;
+            const int idx = head + 8 * (v0 + found * kArgThreads) + e0;
+            if (e0 >= 0 && beats32(m, idx, best, bi)) {
+                best = m;
+                bi = idx;
             }
+        }
+    }
+    if (tid < head) {
+        const float v = h2f(src[tid]);
+        if (v == v && beats32(v, tid, best, bi)) {
+            best = v;
+            bi = tid;
+        }
+    }
+    if (tail0 + tid < n) {
+        const float v = h2f(src[tail0 + tid]);
+        if (v == v && beats32(v, tail0 + tid, best, bi)) {
+            best = v;
+            bi = tail0 + tid;
         }
     }
 #pragma unroll
     for (int o = kWave / 2; o > 0; o >>= 1) {
         const float v2 = __shfl_xor(best, o);
-        const int64_t i2 = __shfl_xor(bi, o);
-        if (beats(v2, i2, best, bi)) {
+        const int i2 = __shfl_xor(bi, o);
+        if (beats32(v2, i2, best, bi)) {
             best = v2;
             bi = i2;
         }
@@ -297,13 +325,13 @@ __global__ __launch_bounds__(kArgThreads) void argmax_kernel(const uint16_t* y, 
     __syncthreads();
     if (tid == 0) {
         float v = s_v[0];
-        int64_t i = s_i[0];
+        int i = s_i[0];
         for (int w = 1; w < kWaves; ++w)
-            if (beats(s_v[w], s_i[w], v, i)) {
+            if (beats32(s_v[w], s_i[w], v, i)) {
                 v = s_v[w];
                 i = s_i[w];
             }
-        *out = (int32_t)i;
+        *out = i;
     }
 }
 
@@ -475,7 +503,7 @@ extern "C" wq_status wq_fused_linears(const wq_fused_linear* linears, int64_t co
     }
     if (argmax) {
         const wq_fused_linear& last = lin[count - 1];
-        hipLaunchKernelGGL(argmax_kernel, dim3(1), dim3(kArgThreads), 0, s, last.y, last.N, argmax);
+        hipLaunchKernelGGL(argmax_kernel, dim3(1), dim3(kArgThreads), 0, s, last.y, (int)last.N, argmax);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return err(WQ_ERR_HIP, "%s: argmax: HIP error %d (%s)", fn, (int)e, hipGetErrorString(e));
     }

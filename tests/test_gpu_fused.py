@@ -321,3 +321,18 @@ def test_fused_argmax_edge_cases(n, offset):
         assert got == _first_max_ignoring_nan(c), (n, offset, got)
         if not np.isnan(c.astype(np.float32)).any():
             assert got == fo.argmax_first(c)
+
+
+def test_fused_argmax_nan_and_neg_inf_mix():
+    """-inf as the largest value behind vectors of NaN, and a maximum that
+    appears again in a later vector and in the scalar tail."""
+    announce("argmax NaN / -inf mix")
+    n = 8 * 1024 * 3 + 5
+    v = np.full(n, np.nan, dtype=np.float16)
+    v[8 * 1024 * 2 + 3] = -np.inf
+    v[8 * 1024 * 2 + 9] = -np.inf
+    assert _argmax_through_residual(v, 0) == 8 * 1024 * 2 + 3
+    w = _h(np.random.default_rng(3).standard_normal(n))
+    w[[40, 8 * 1024 + 40, n - 1]] = np.float16(50.0)
+    for off in (0, 3):
+        assert _argmax_through_residual(w, off) == 40
