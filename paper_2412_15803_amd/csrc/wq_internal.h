@@ -26,6 +26,15 @@ hipError_t launch_gemv(const uint32_t* packed, const uint16_t* scales,
 // vector ALUs.
 constexpr int kMatrixCoreMinM = 8;
 
+// Largest batch of the small-batch kernels; larger ones (prompts) run the
+// tiled prefill GEMM.
+constexpr int kMaxSmallBatchM = 64;
+
+// y[M][N] for M > kMaxSmallBatchM: 128 x 128 tiles on the matrix cores.
+bool prefill_fits(int64_t n, int64_t k, int64_t m);
+hipError_t launch_prefill(const uint32_t* packed, const uint16_t* scales, const uint16_t* x, uint16_t* y,
+                          int64_t n, int64_t k, int64_t m, hipStream_t stream);
+
 // WQ_SMALL_BATCH_VECTOR=1 in the environment sends every small batch to the
 // vector kernel (for comparing the two paths; read at every call).
 bool vector_small_batch();

@@ -366,7 +366,7 @@ hipError_t launch_gemv(const uint32_t* packed, const uint16_t* scales, const uin
         WQ_M1_CASE(16, 1) WQ_M1_CASE(16, 3) WQ_M1_CASE(16, 5) WQ_M1_CASE(16, 7)
 #undef WQ_M1_CASE
     }
-    if (m >= 2 && m <= 64 && fits_rsrc(n, ng)) {
+    if (m >= 2 && m <= kMaxSmallBatchM && fits_rsrc(n, ng)) {
         // Matrix cores from 8 batch rows on (measured faster than the vector
         // kernel there); below that, or when asked to, the vector kernel in
         // passes of up to 8 rows.
@@ -382,6 +382,8 @@ hipError_t launch_gemv(const uint32_t* packed, const uint16_t* scales, const uin
         }
         return hipSuccess;
     }
+    // Prompt-sized batches: the tiled matrix-core GEMM.
+    if (m > kMaxSmallBatchM && prefill_fits(n, k, m)) return launch_prefill(packed, scales, x, y, n, k, m, stream);
     constexpr int MC = 4;
     const int64_t mchunks = (m + MC - 1) / MC;
     const int64_t waves = n * mchunks;

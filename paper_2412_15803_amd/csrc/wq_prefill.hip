@@ -1,0 +1,181 @@
+// Prefill (many rows of x at once) 4-bit GEMM on the matrix cores:
+// y[M][N] = x[M][K] dequant(W)^T for M above the small-batch range.  Prompt
+// processing runs the same quantized linears over every prompt token; the
+// tiling is the operator-level GEMM tiling the paper's compiler applies
+// (Sec. 2.3), written for gfx950's v_mfma_f32_16x16x32_f16.
+//
+// Tiles.  A 256-thread block computes a 128 (x rows) x 128 (weight rows)
+// tile of y over K in stages of 64.  Per stage every thread loads four
+// 16-byte pieces of x and one 16-byte group of codes (32 weights) with its
+// scale, then writes them to LDS: x as is, the codes dequantized (exact
+// q - 8, then times the scale, rounded once to fp16 as on the small-batch
+// matrix-core path).  Within every 8-element piece both operands are stored
+// in the order (0, 4, 1, 5, 2, 6, 3, 7) in which a code word dequantizes, so
+// the fragments read back from LDS line up without further shuffles.  LDS is
+// double-buffered: the global loads of stage s + 1 are in flight while
+// stage s is multiplied, and one barrier per stage separates writing a
+// buffer from reading it.
+//
+// Waves.  The four waves form a 2 x 2 grid, each owning 64 x 64 of the tile:
+// 4 x 4 accumulators of 16 x 16, i.e. 16 multiplies per 32-deep k step.
+// Lane layouts (as on the small-batch path): A lane l holds
+// A[l % 16][8 (l / 16) + v], B lane l holds B[8 (l / 16) + v][l % 16], the
+// result lane l holds D[4 (l / 16) + v][l % 16].
+//
+// Edges.  x rows past M and k past K load zeros; weight rows past N and
+// groups past K get scale 0 (zero weights); results past M or N are not
+// stored.
+#include "wq_device.h"
+#include "wq_internal.h"
+
+namespace wq {
+namespace {
+
+using namespace dev;
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef float float4v __attribute__((ext_vector_type(4)));
+
+constexpr int kBM = 128;
+constexpr int kBN = 128;
+constexpr int kBK = 64;
+constexpr int kThreads = 256;
+constexpr int kRow = kBK + 8;  // LDS row in halves: 144 bytes, which spreads rows over the banks
+
+struct Stage {
+    uint16_t a[kBM][kRow];  // x, 8-element pieces in dequantization order
+    uint16_t b[kBN][kRow];  // fp16 weights (q - 8) * s, same order
+};
+
+// 8 consecutive x values (k .. k + 7) in the order a code word dequantizes:
+// (0, 4), (1, 5), (2, 6), (3, 7).
+__device__ __forceinline__ u32x4 to_dequant_order(const u32x4 d) {
+    u32x4 r;
+    r.x = __builtin_amdgcn_perm(d.z, d.x, 0x05040100u);
+    r.y = __builtin_amdgcn_perm(d.z, d.x, 0x07060302u);
+    r.z = __builtin_amdgcn_perm(d.w, d.y, 0x05040100u);
+    r.w = __builtin_amdgcn_perm(d.w, d.y, 0x07060302u);
+    return r;
+}
+
+__global__ __launch_bounds__(kThreads) void prefill_kernel(const u32x4* __restrict__ packed,
+                                                           const uint16_t* __restrict__ scales,
+                                                           const uint16_t* __restrict__ x, uint16_t* __restrict__ y,
+                                                           int m, int n, int k, int blocks_m) {
+    __shared__ __align__(16) Stage st[2];
+    const int tid = threadIdx.x;
+    const int lane = tid & (kWave - 1);
+    const int wave = tid / kWave;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int bid = blockIdx.x;
+    const int m0 = (bid % blocks_m) * kBM;
+    const int n0 = (bid / blocks_m) * kBN;
+    const int ng = k / kGroup;
+    const int stages = (k + kBK - 1) / kBK;
+
+    // This thread's share of a stage's global loads.
+    u32x4 ra[4];
+    u32x4 rb;
+    uint32_t rs;
+    const int bn = tid >> 1, bgrp = tid & 1;  // weight row and group (of two) of the B piece
+    auto load_stage = [&](int s) {
+        const int k0 = s * kBK;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int c = tid + kThreads * i;
+            const int row = c >> 3, kc = c & 7;
+            const int gm = m0 + row, gk = k0 + 8 * kc;
+            ra[i] = (gm < m && gk < k)
+                        ? *reinterpret_cast<const WQ_GLOBAL u32x4*>(gbl(x) + (int64_t)gm * k + gk)
+                        : u32x4{0u, 0u, 0u, 0u};
+        }
+        const int gn = n0 + bn, g = 2 * s + bgrp;
+        const bool ok = gn < n && g < ng;
+        rb = ok ? gbl(packed)[(int64_t)gn * ng + g] : u32x4{0x88888888u, 0x88888888u, 0x88888888u, 0x88888888u};
+        rs = ok ? (uint32_t)gbl(scales)[(int64_t)gn * ng + g] : 0u;
+    };
+    auto store_stage = [&](Stage& S) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int c = tid + kThreads * i;
+            const int row = c >> 3, kc = c & 7;
+            *reinterpret_cast<u32x4*>(&S.a[row][8 * kc]) = to_dequant_order(ra[i]);
+        }
+        const half2v sc = as_h2(rs | (rs << 16));
+        const uint32_t w[4] = {rb.x, rb.y, rb.z, rb.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            half2v q[4];
+            dequant_word(w[j], q);
+            const u32x4 o = {__builtin_bit_cast(uint32_t, q[0] * sc), __builtin_bit_cast(uint32_t, q[1] * sc),
+                             __builtin_bit_cast(uint32_t, q[2] * sc), __builtin_bit_cast(uint32_t, q[3] * sc)};
+            *reinterpret_cast<u32x4*>(&S.b[bn][32 * bgrp + 8 * j]) = o;
+        }
+    };
+
+    float4v acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = float4v{0.0f, 0.0f, 0.0f, 0.0f};
+
+    const int r = lane & 15, c = lane >> 4;
+    load_stage(0);
+    store_stage(st[0]);
+    __syncthreads();
+    for (int s = 0; s < stages; ++s) {
+        const bool more = s + 1 < stages;
+        if (more) load_stage(s + 1);
+        const Stage& S = st[s & 1];
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            half8 fa[4], fb[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                fa[i] = *reinterpret_cast<const half8*>(&S.a[64 * wm + 16 * i + r][32 * ks + 8 * c]);
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                fb[j] = *reinterpret_cast<const half8*>(&S.b[64 * wn + 16 * j + r][32 * ks + 8 * c]);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+        }
+        if (more) store_stage(st[(s + 1) & 1]);
+        __syncthreads();
+    }
+
+    // D[4 c + v][r] of tile (i, j): x row 64 wm + 16 i + 4 c + v, weight row 64 wn + 16 j + r.
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int gn = n0 + 64 * wn + 16 * j + r;
+            if (gn >= n) continue;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int gm = m0 + 64 * wm + 16 * i + 4 * c + v;
+                if (gm < m) gbl(y)[(int64_t)gm * n + gn] = __half_as_ushort(__float2half_rn(acc[i][j][v]));
+            }
+        }
+    }
+}
+
+}  // namespace
+
+bool prefill_fits(int64_t n, int64_t k, int64_t m) {
+    const int64_t blocks = ((m + kBM - 1) / kBM) * ((n + kBN - 1) / kBN);
+    return n <= INT32_MAX && k <= INT32_MAX && m <= INT32_MAX && blocks <= INT32_MAX;
+}
+
+hipError_t launch_prefill(const uint32_t* packed, const uint16_t* scales, const uint16_t* x, uint16_t* y,
+                          int64_t n, int64_t k, int64_t m, hipStream_t stream) {
+    const int64_t blocks_m = (m + kBM - 1) / kBM;
+    const int64_t blocks = blocks_m * ((n + kBN - 1) / kBN);
+    hipLaunchKernelGGL(prefill_kernel, dim3((unsigned)blocks), dim3(kThreads), 0, stream,
+                       reinterpret_cast<const u32x4*>(packed), scales, x, y, (int)m, (int)n, (int)k, (int)blocks_m);
+    return hipGetLastError();
+}
+
+}  // namespace wq
