@@ -52,6 +52,10 @@ def parse_args():
                     help="time only the dependent decode step (for profiling the fused kernels)")
     ap.add_argument("--dependent-ctx", type=int, default=0,
                     help="with --dependent-only: cached tokens per layer for attention (0: linears only)")
+    ap.add_argument("--prefill-only", action="store_true",
+                    help="time only the prefill GEMM shapes (for profiling its kernel)")
+    ap.add_argument("--prefill-config", type=int, default=None,
+                    help="with --prefill-only: time only this entry of PREFILL_CONFIGS")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the per-shape figures (single linears, small batches, 8B-class step)")
     return ap.parse_args()
@@ -440,6 +444,72 @@ def time_dependent_step(lins, device, seed, ctx=4096, steps=20, reps=3):
             "finite_logits": bool(torch.isfinite(ref_logits).all().item())}
 
 
+MFMA_F16_PEAK_TFLOPS = 2500.0  # MI355X dense fp16 matrix-core peak
+
+PREFILL_CONFIGS = (
+    # (label, N, K, M): prompt-sized batches of one linear
+    ("3B gate_up 16384x3072, M=2048 prompt tokens", 16384, 3072, 2048),
+    ("3B down 3072x8192, M=2048", 3072, 8192, 2048),
+    ("3B lm_head 128256x3072, M=2048", 128256, 3072, 2048),
+    ("8B gate_up 28672x4096, M=512", 28672, 4096, 512),
+)
+
+
+def time_prefill(n, k, m, gen, device, reps=10):
+    """wq_gemv on M rows of x (the tiled matrix-core kernel): device time per
+    call from events around `reps` back-to-back calls."""
+    import torch
+
+    from paper_2412_15803_amd import wq
+
+    packed, scales = random_linear(n, k, gen, device)
+    x = torch.randn((m, k), generator=gen, device=device).to(torch.float16)
+    y = torch.empty((m, n), dtype=torch.float16, device=device)
+    for _ in range(2):
+        wq.wq_gemv(packed, scales, x, y)
+    torch.cuda.synchronize()
+    a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        wq.wq_gemv(packed, scales, x, y)
+    e.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(e) / reps
+    tflops = 2.0 * m * n * k / (ms * 1e-3) / 1e12
+    del packed, scales, x, y
+    torch.cuda.empty_cache()
+    return {"us": round(ms * 1e3, 1), "TFLOP_s": round(tflops, 1), "frac": round(tflops / MFMA_F16_PEAK_TFLOPS, 4)}
+
+
+def prefill_configs(device, seed, only=None):
+    """Prompt processing (M > 64 rows of x): the tiled fp16 matrix-core GEMM
+    with the 4-bit weights dequantized per tile; TFLOP/s and the fraction of
+    the dense fp16 matrix-core peak.  Also the whole 3B-class step's 113
+    linears over a 2048-token prompt."""
+    import torch
+
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed + 31)
+    res = {"method": "wq_gemv / wq_decode_linears with M prompt rows, random codes and scales, device time from "
+                     "events around back-to-back calls; flops = 2 M N K", "peak_TFLOP_s": MFMA_F16_PEAK_TFLOPS}
+    for i, (label, n, k, m) in enumerate(PREFILL_CONFIGS):
+        if only is not None and i != only:
+            continue
+        res[label] = time_prefill(n, k, m, gen, device)
+    if only is None:
+        from paper_2412_15803_amd import workloads as wl
+
+        m = 2048
+        steps3 = [(lin.n, lin.k) for lin in wl.LLAMA3B_LAYER] * 28 + [(wl.LLAMA3B_LM_HEAD.n, wl.LLAMA3B_LM_HEAD.k)]
+        flops = sum(2.0 * m * n * k for n, k in steps3)
+        got = time_step_batches(steps3, [m], gen, device, 3, 1)[m]
+        tflops = flops / (got["us"] * 1e-6) / 1e12
+        res["3B step, 113 linears, M=2048 prompt tokens (one wq_decode_linears call)"] = {
+            "us": got["us"], "prompt_tokens_per_s": got["tokens_per_s"], "TFLOP_s": round(tflops, 1),
+            "frac": round(tflops / MFMA_F16_PEAK_TFLOPS, 4)}
+    return res
+
+
 # Counter summaries of the split kernel, by ATTN_CONFIGS index.
 ATTN_PROFILES = {0: "paged_attention_3b_ctx4096.md", 1: "paged_attention_3b_ctx32768.md"}
 ATTN_SOURCES = ("wq_attention.hip", "wq_device.h")
@@ -511,6 +581,7 @@ def per_config(device, seed):
     for m, v in time_step_batches(steps8, [1, 4, 8, 16], gen, device, 20, 3).items():
         res[f"8B step M={m} (one wq_decode_linears call, 129 linears)"] = v
     res["paged decode attention"] = attention_configs(device, seed)
+    res["prefill"] = prefill_configs(device, seed)
     return res
 
 
@@ -555,6 +626,13 @@ def main():
         sys.exit(1)
     device = torch.device("cuda:0")
     wq.lib()  # fail loudly if the HIP library is missing
+
+    if args.prefill_only:
+        if args.copy_probe_mib:
+            copy_probe(args.copy_probe_mib, device)
+        log("timing the prefill GEMM shapes")
+        print(json.dumps({"prefill": prefill_configs(device, args.seed, args.prefill_config)}), flush=True)
+        return
 
     if args.attention_only:
         if args.copy_probe_mib:

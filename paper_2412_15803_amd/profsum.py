@@ -100,6 +100,8 @@ def summarise(args):
         f"| scale factors applied (fetch / write) | {f_scale:.4f} / {w_scale:.4f} |",
         f"| HBM traffic per launch, scaled (fetch + write bytes) | {fetch_b:,.0f} + {write_b:,.0f} = {traffic:,.0f} |",
         f"| traffic / algorithmic bytes | {traffic / args.algo_bytes:.4f} |",
+        *([f"| flops per launch; achieved (flops / avg duration) | {args.flops:,} ; "
+           f"{args.flops / (avg * 1e-6) / 1e12:.1f} TFLOP/s |"] if args.flops else []),
         *others,
         "",
         "Machine-readable (read by bench.py; valid only for this source hash):",
@@ -144,6 +146,7 @@ def main():
     ap.add_argument("--command", action="append", required=True)
     ap.add_argument("--title", default="Kernel trace and HBM traffic")
     ap.add_argument("--also", action="append", help="another kernel to list (durations and traffic)")
+    ap.add_argument("--flops", type=int, default=0, help="flops per launch, for a matrix-core kernel")
     ap.add_argument("--sources", default=None,
                     help="comma-separated csrc/ files whose hash marks the summary (default: the step kernel's)")
     ap.add_argument("--out", required=True)
