@@ -141,9 +141,45 @@ __device__ __forceinline__ void mb_issue(MbBuf<MB>& b, const LinearRsrc& r, int6
     __builtin_amdgcn_sched_barrier(0);
 }
 
+// Sum each of V per-lane values (V = 8, 16 or 32) over the 64 lanes, leaving
+// value j + r V / 4 (j < V / 4) in lane 16 r + j.  Two swap levels halve the
+// values per register while folding lanes l, l + 32 and then 16-lane rows
+// 0 + 1 and 2 + 3 together (v_permlane32_swap exchanges the upper 32 lanes of
+// its first operand with the lower 32 of its second, v_permlane16_swap the
+// odd 16-lane rows of the first with the even rows of the second); a 16-lane
+// DPP sum finishes each register and V / 4 selects gather the results.
+// About 2.5 operations per value instead of a 6-step reduction each.
+template <int V>
+__device__ __forceinline__ float transpose_reduce(const float (&v)[V], int lane) {
+    float s[V / 2];
+#pragma unroll
+    for (int j = 0; j < V / 2; ++j) {
+        // (A non-const result: with `const auto` this compiler reads element 0
+        // for both elements of the returned pair.)
+        auto p = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, v[j]),
+                                                   __builtin_bit_cast(uint32_t, v[j + V / 2]), false, false);
+        const uint32_t lo = p[0], hi = p[1];
+        s[j] = __builtin_bit_cast(float, lo) + __builtin_bit_cast(float, hi);
+    }
+    float t[V / 4];
+#pragma unroll
+    for (int j = 0; j < V / 4; ++j) {
+        auto q = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(uint32_t, s[j]),
+                                                   __builtin_bit_cast(uint32_t, s[j + V / 4]), false, false);
+        const uint32_t even = q[0], odd = q[1];
+        t[j] = segment_sum<16>(__builtin_bit_cast(float, even) + __builtin_bit_cast(float, odd));
+    }
+    float r = t[0];
+#pragma unroll
+    for (int j = 1; j < V / 4; ++j) r = (lane & 15) == j ? t[j] : r;
+    return r;
+}
+
 template <int MB>
 __device__ __forceinline__ void mb_compute(const MbBuf<MB>& b, const half2v (&xr)[MB][16], float* part,
                                            int rel, int nrows, int lane) {
+    constexpr int V = kMbU * MB;  // (row, batch row) sums of one step
+    float v[V];
 #pragma unroll
     for (int u = 0; u < kMbU; ++u) {
         float acc[MB];
@@ -161,11 +197,15 @@ __device__ __forceinline__ void mb_compute(const MbBuf<MB>& b, const half2v (&xr
         }
         const float sc = __half2float(__ushort_as_half((uint16_t)b.s[u]));
 #pragma unroll
-        for (int i = 0; i < MB; ++i) {
-            const float tot = segment_sum<kWave>(sc * acc[i]);
-            if (lane == kWave - 1 && u < nrows) part[(rel + u) * MB + i] += tot;
-        }
+        for (int i = 0; i < MB; ++i) v[u * MB + i] = sc * acc[i];
     }
+    // One reduction for the whole step; lane 16 r + j then holds the sum of
+    // value j + r V / 4, i.e. row idx / MB, batch row idx % MB.
+    const float tot = transpose_reduce<V>(v, lane);
+    const int j = lane & 15;
+    const int idx = j + (lane >> 4) * (V / 4);
+    const int u = idx / MB, i = idx % MB;
+    if (j < V / 4 && u < nrows) part[(rel + u) * MB + i] += tot;
 }
 
 // Rows [rb, re) of one linear (re - rb <= kMbRows), batch rows [0, m).
