@@ -254,6 +254,7 @@ struct DecodeWorkspace {
     bool stage_pending = false;
     std::vector<unsigned char> uploaded; // bytes of the plan now in d_plan
     int waves4 = 0, waves8 = 0;          // resident waves of the two kernel variants
+    int64_t mb_waves[3] = {0, 0, 0};     // target waves of the vector small-batch kernel, m <= 2, 4, 8
 };
 
 std::mutex g_ws_mu;
@@ -269,6 +270,8 @@ wq_status get_workspace(const char* fn, hipStream_t stream, DecodeWorkspace*& ou
         if ((e = hipEventCreateWithFlags(&fresh->staged, hipEventDisableTiming)) != hipSuccess) return hip_status(fn, e);
         if ((e = wq::grouped_capacity(4, device, fresh->waves4)) != hipSuccess) return hip_status(fn, e);
         if ((e = wq::grouped_capacity(8, device, fresh->waves8)) != hipSuccess) return hip_status(fn, e);
+        for (int i = 0; i < 3; ++i)
+            if ((e = wq::mb_target_waves(2 << i, device, fresh->mb_waves[i])) != hipSuccess) return hip_status(fn, e);
         // Tuning override: fewer waves than the device holds (never more,
         // since every wave owns a fixed share of the work).
         if (const char* env = std::getenv("WQ_GROUPED_WAVES")) {
@@ -277,6 +280,12 @@ wq_status get_workspace(const char* fn, hipStream_t stream, DecodeWorkspace*& ou
                 fresh->waves4 = std::min(fresh->waves4, w);
                 fresh->waves8 = std::min(fresh->waves8, w);
             }
+        }
+        // Tuning override: the vector small-batch kernel's target wave count.
+        if (const char* env = std::getenv("WQ_MB_WAVES")) {
+            const long long w = std::atoll(env);
+            if (w > 0)
+                for (int64_t& v : fresh->mb_waves) v = w;
         }
         ws = fresh.release();
     }
@@ -392,12 +401,17 @@ BatchPlan plan_batch_group(const std::vector<wq_linear>& lin, const Group& g, st
 }
 
 // 2 <= M < 8 on the vector ALUs: one launch per dependency group and 8
-// batch rows; waves own fixed-size row runs of one linear each.
-BatchPlan plan_vector_group(const std::vector<wq_linear>& lin, const Group& g, std::vector<unsigned char>& bytes) {
+// batch rows; waves own row runs of one linear each.  The runs are sized so
+// that every wave streams about the same number of (row, padded group)
+// pairs, `target` waves in all (fixed-size runs would give a K = 8192 wave
+// 2.7 times the work of a K = 3072 one, and the CUs holding those waves
+// would set the time).
+BatchPlan plan_vector_group(const std::vector<wq_linear>& lin, const Group& g, int64_t target,
+                            std::vector<unsigned char>& bytes) {
     const int count = g.end - g.begin;
-    int64_t total_rows = 0;
-    for (int i = 0; i < count; ++i) total_rows += lin[g.begin + i].N;
-    const int rows = wq::mb_rows_per_wave(total_rows);
+    int64_t work = 0;
+    for (int i = 0; i < count; ++i) work += lin[g.begin + i].N * wq::mb_padded_groups(lin[g.begin + i].K / 32);
+    const int64_t per_wave = (work + target - 1) / target;
     std::vector<wq::DecodeEntry> ents(count, wq::DecodeEntry{});
     int64_t waves = 0;
     for (int i = 0; i < count; ++i) {
@@ -409,9 +423,9 @@ BatchPlan plan_vector_group(const std::vector<wq_linear>& lin, const Group& g, s
         e.y = l.y;
         e.n = l.N;
         e.ng = (int32_t)(l.K / 32);
-        e.pad = rows;
+        e.pad = wq::mb_rows_for_work(per_wave, e.ng);
         e.first_step = waves;
-        e.steps = (l.N + rows - 1) / rows;
+        e.steps = (l.N + e.pad - 1) / e.pad;
         waves += e.steps;
     }
     BatchPlan bp;
@@ -437,7 +451,8 @@ wq_status decode_grouped_batch(const char* fn, const std::vector<wq_linear>& lin
     std::vector<BatchPlan> plans(groups.size());
     for (size_t i = 0; i < groups.size(); ++i)
         if (groups[i].grouped)
-            plans[i] = matrix ? plan_batch_group(lin, groups[i], bytes) : plan_vector_group(lin, groups[i], bytes);
+            plans[i] = matrix ? plan_batch_group(lin, groups[i], bytes)
+                              : plan_vector_group(lin, groups[i], ws->mb_waves[m <= 2 ? 0 : m <= 4 ? 1 : 2], bytes);
     if (!bytes.empty() && (st = upload_plan(fn, ws, bytes, stream)) != WQ_OK) return st;
     for (size_t i = 0; i < groups.size(); ++i) {
         const Group& g = groups[i];

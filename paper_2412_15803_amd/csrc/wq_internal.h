@@ -92,11 +92,23 @@ hipError_t launch_grouped_mfma(const DecodeEntry* entries, int count, int64_t bl
 
 // Small-batch decode step below kMatrixCoreMinM rows: independent linears in
 // one launch of the vector kernel.  Entry i owns waves [first_step,
-// first_step + steps) of the grid, `pad` rows each (mb_rows_per_wave of the
-// launch's total rows); batch rows [m0, m0 + m), m <= 8.
+// first_step + steps) of the grid, `pad` rows each (a multiple of 8, at most
+// 256); batch rows [m0, m0 + m), m <= 8.
 hipError_t launch_grouped_mb(const DecodeEntry* entries, int count, int64_t waves, int64_t m0, int m,
                              hipStream_t stream);
-int mb_rows_per_wave(int64_t total_rows);
+// Waves to split such a launch into for m batch rows (m <= 8) on `device`:
+// a few times what the device holds at once.
+hipError_t mb_target_waves(int m, int device, int64_t& waves);
+// Rows per wave for a linear of ng groups per row when each wave is to
+// stream about `work` (row, padded group) pairs.
+int mb_rows_for_work(int64_t work, int64_t ng);
+
+// The vector small-batch kernel walks a row's groups in 32-group tiles, two
+// row sets per wave, when those pad the row less than 64-group tiles do.
+__host__ __device__ inline bool mb_two_sets(int64_t ng) { return (ng + 31) / 32 * 32 < (ng + 63) / 64 * 64; }
+__host__ __device__ inline int64_t mb_padded_groups(int64_t ng) {
+    return mb_two_sets(ng) ? (ng + 31) / 32 * 32 : (ng + 63) / 64 * 64;
+}
 
 // Largest groups-per-lane of the grouped kernel (K <= 16384).
 constexpr int kDecodeMaxGpl = 8;

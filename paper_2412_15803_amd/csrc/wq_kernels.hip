@@ -112,15 +112,20 @@ __global__ __launch_bounds__(kBlock) void gemv_m1_kernel(const u32x4* packed, co
 // ------------------------------------------------ small batches, vector ALUs
 //
 // For 2 <= M <= 8 batch rows per pass.  A wave owns rows [rb, re) (at most
-// kMbRows) and walks the row's groups in tiles of 64: lane l takes group
-// 64 kt + l of every row.  Per tile it loads x of its group for the MB batch
-// rows into registers (pre-paired like the batch-1 kernels), then streams
-// its rows kMbU at a time through two register buffers (buffer-resource
-// loads, as in the batch-1 kernels).  Each row's MB dot products are reduced
-// across the wave with DPP, and lane 63 adds them to fp32 partial sums in
-// LDS; after the last tile the partials are rounded once to fp16.
+// kMbRows) and walks the row's groups in tiles: either 64 groups, lane l
+// taking group 64 kt + l of every row, or (when a row's group count is an odd
+// multiple of 32, or below 32) 32 groups, lanes 0-31 and 32-63 then taking
+// group 32 kt + l % 32 of two different row sets.  Per tile it loads x of
+// its group for the MB batch rows into registers (pre-paired like the
+// batch-1 kernels), then streams its rows kMbU (per row set) at a time
+// through two register buffers (buffer-resource loads, as in the batch-1
+// kernels).  The dot products of one step are reduced across the lanes of
+// each row set in one transposed reduction, and one lane per sum adds it to
+// fp32 partial sums in LDS; after the last tile the partials are rounded
+// once to fp16.
 constexpr int kMbRows = 256;
 constexpr int kMbU = 4;
+constexpr int kMbStep = 2 * kMbU;  // rows per wave are a multiple of a step of either tiling
 
 template <int MB>
 struct MbBuf {
@@ -128,57 +133,72 @@ struct MbBuf {
     uint32_t s[kMbU];
 };
 
-template <int MB>
+// Issue the loads of one step: rows row0 + h kMbU + u (u < kMbU) for each of
+// the H row sets, the tile's T = 64 / H groups per row.  Lane l takes group
+// T kt + l % T of row set l / T.
+template <int MB, int H>
 __device__ __forceinline__ void mb_issue(MbBuf<MB>& b, const LinearRsrc& r, int64_t row0, int kt, int ng,
                                          int lane) {
+    constexpr int T = kWave / H;
+    const uint32_t lg = (uint32_t)(lane % T + (lane / T) * kMbU * ng);  // relative to the step's first group
 #pragma unroll
     for (int u = 0; u < kMbU; ++u) {
-        const uint32_t go = (uint32_t)((row0 + u) * ng + 64 * kt);
-        b.w[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r.w, lane * 16, go * 16, 0));
-        b.s[u] = __builtin_amdgcn_raw_buffer_load_b16(r.s, lane * 2, go * 2, 0);
+        const uint32_t go = (uint32_t)((row0 + u) * ng + T * kt);
+        b.w[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r.w, lg * 16, go * 16, 0));
+        b.s[u] = __builtin_amdgcn_raw_buffer_load_b16(r.s, lg * 2, go * 2, 0);
     }
     asm volatile("" ::: "memory");
     __builtin_amdgcn_sched_barrier(0);
 }
 
-// Sum each of V per-lane values (V = 8, 16 or 32) over the 64 lanes, leaving
-// value j + r V / 4 (j < V / 4) in lane 16 r + j.  Two swap levels halve the
-// values per register while folding lanes l, l + 32 and then 16-lane rows
-// 0 + 1 and 2 + 3 together (v_permlane32_swap exchanges the upper 32 lanes of
-// its first operand with the lower 32 of its second, v_permlane16_swap the
-// odd 16-lane rows of the first with the even rows of the second); a 16-lane
-// DPP sum finishes each register and V / 4 selects gather the results.
-// About 2.5 operations per value instead of a 6-step reduction each.
-template <int V>
+// Sum each of V per-lane values (V = 8, 16 or 32) over the lanes of each of
+// the H row sets (64 lanes when H = 1, 32 when H = 2), leaving value
+// j + r W (j < W, W = V / 4 when H = 1, V / 2 when H = 2) in lane 16 r + j;
+// with H = 2, values from V on belong to the second row set.  Swap levels
+// halve the values per register while folding lanes l, l + 32 (only when
+// both halves hold the same rows) and then 16-lane rows 0 + 1 and 2 + 3
+// together (v_permlane32_swap exchanges the upper 32 lanes of its first
+// operand with the lower 32 of its second, v_permlane16_swap the odd 16-lane
+// rows of the first with the even rows of the second); a 16-lane DPP sum
+// finishes each register and W selects gather the results.  About 2.5
+// operations per value instead of a 6-step reduction each.
+template <int V, int H>
 __device__ __forceinline__ float transpose_reduce(const float (&v)[V], int lane) {
-    float s[V / 2];
+    constexpr int V1 = H == 1 ? V / 2 : V;
+    constexpr int W = V1 / 2;
+    float s[V1];
+    if constexpr (H == 1) {
 #pragma unroll
-    for (int j = 0; j < V / 2; ++j) {
-        // (A non-const result: with `const auto` this compiler reads element 0
-        // for both elements of the returned pair.)
-        auto p = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, v[j]),
-                                                   __builtin_bit_cast(uint32_t, v[j + V / 2]), false, false);
-        const uint32_t lo = p[0], hi = p[1];
-        s[j] = __builtin_bit_cast(float, lo) + __builtin_bit_cast(float, hi);
+        for (int j = 0; j < V1; ++j) {
+            // (A non-const result: with `const auto` this compiler reads
+            // element 0 for both elements of the returned pair.)
+            auto p = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, v[j]),
+                                                       __builtin_bit_cast(uint32_t, v[j + V1]), false, false);
+            const uint32_t lo = p[0], hi = p[1];
+            s[j] = __builtin_bit_cast(float, lo) + __builtin_bit_cast(float, hi);
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < V1; ++j) s[j] = v[j];
     }
-    float t[V / 4];
+    float t[W];
 #pragma unroll
-    for (int j = 0; j < V / 4; ++j) {
+    for (int j = 0; j < W; ++j) {
         auto q = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(uint32_t, s[j]),
-                                                   __builtin_bit_cast(uint32_t, s[j + V / 4]), false, false);
+                                                   __builtin_bit_cast(uint32_t, s[j + W]), false, false);
         const uint32_t even = q[0], odd = q[1];
         t[j] = segment_sum<16>(__builtin_bit_cast(float, even) + __builtin_bit_cast(float, odd));
     }
     float r = t[0];
 #pragma unroll
-    for (int j = 1; j < V / 4; ++j) r = (lane & 15) == j ? t[j] : r;
+    for (int j = 1; j < W; ++j) r = (lane & 15) == j ? t[j] : r;
     return r;
 }
 
-template <int MB>
+template <int MB, int H>
 __device__ __forceinline__ void mb_compute(const MbBuf<MB>& b, const half2v (&xr)[MB][16], float* part,
                                            int rel, int nrows, int lane) {
-    constexpr int V = kMbU * MB;  // (row, batch row) sums of one step
+    constexpr int V = kMbU * MB;  // (row, batch row) sums of one row set
     float v[V];
 #pragma unroll
     for (int u = 0; u < kMbU; ++u) {
@@ -200,30 +220,41 @@ __device__ __forceinline__ void mb_compute(const MbBuf<MB>& b, const half2v (&xr
         for (int i = 0; i < MB; ++i) v[u * MB + i] = sc * acc[i];
     }
     // One reduction for the whole step; lane 16 r + j then holds the sum of
-    // value j + r V / 4, i.e. row idx / MB, batch row idx % MB.
-    const float tot = transpose_reduce<V>(v, lane);
+    // value idx = j + r W: row set idx / V, row (idx % V) / MB of it, batch
+    // row idx % MB.
+    constexpr int W = H == 1 ? V / 4 : V / 2;
+    const float tot = transpose_reduce<V, H>(v, lane);
     const int j = lane & 15;
-    const int idx = j + (lane >> 4) * (V / 4);
-    const int u = idx / MB, i = idx % MB;
-    if (j < V / 4 && u < nrows) part[(rel + u) * MB + i] += tot;
+    const int idx = j + (lane >> 4) * W;
+    const int row = (idx / V) * kMbU + (idx % V) / MB, i = idx % MB;
+    if (j < W && row < nrows) part[(rel + row) * MB + i] += tot;
 }
 
-// Rows [rb, re) of one linear (re - rb <= kMbRows), batch rows [0, m).
-template <int MB>
+// Rows [rb, re) of one linear (re - rb <= kMbRows), batch rows [0, m), in
+// tiles of T = 64 / H groups and steps of H kMbU rows.  The steps of all
+// tiles form one stream through the two buffers: the loads of a tile's first
+// steps are issued while the previous tile's last steps are computed, and x
+// of the next tile is loaded right after the last step that reads the
+// current one (ahead of the next weight loads, so that waiting for x never
+// waits for those).
+template <int MB, int H>
 __device__ __forceinline__ void mb_range(const void* packed, const uint16_t* scales, const uint16_t* x, uint16_t* y,
                                          int64_t n, int ng, int m, int64_t rb, int64_t re, float* part, int lane) {
+    constexpr int T = kWave / H;
+    constexpr int R = H * kMbU;
     const int nrow = (int)(re - rb);
-    const int64_t steps = (nrow + kMbU - 1) / kMbU;
+    const int steps = (nrow + R - 1) / R;
     const LinearRsrc rs = make_rsrc(packed, scales, (uint32_t)(n * ng * 2));
     const int64_t k = (int64_t)ng * kGroup;
     for (int i = lane; i < nrow * MB; i += kWave) part[i] = 0.0f;
     wave_lds_sync();
 
-    const int ntiles = (ng + 63) / 64;
-    for (int kt = 0; kt < ntiles; ++kt) {
-        const int g = 64 * kt + lane;
+    const int ntiles = (ng + T - 1) / T;
+    const int total = ntiles * steps;
+    half2v xr[MB][16];
+    auto load_x = [&](int kt) {
+        const int g = T * kt + lane % T;
         const bool act = g < ng;
-        half2v xr[MB][16];
 #pragma unroll
         for (int i = 0; i < MB; ++i) {
             const int mi = min(i, m - 1);  // rows past m repeat the last one (never stored)
@@ -231,14 +262,31 @@ __device__ __forceinline__ void mb_range(const void* packed, const uint16_t* sca
 #pragma unroll
             for (int e = 0; e < 16; ++e) xr[i][e] = act ? xr[i][e] : half2v{(_Float16)0.0f, (_Float16)0.0f};
         }
-        MbBuf<MB> a, b;
-        for (int64_t s = -2; s < steps; s += 2) {
-            if (s >= 0) mb_compute<MB>(a, xr, part, (int)(s * kMbU), nrow - (int)(s * kMbU), lane);
-            mb_issue<MB>(a, rs, rb + (s + 2) * kMbU, kt, ng, lane);
-            if (s + 1 >= 0 && s + 1 < steps)
-                mb_compute<MB>(b, xr, part, (int)((s + 1) * kMbU), nrow - (int)((s + 1) * kMbU), lane);
-            mb_issue<MB>(b, rs, rb + (s + 3) * kMbU, kt, ng, lane);
+    };
+    load_x(0);
+    // Issue position (tile ki, step si) and compute position (kc, sc), both
+    // wave-uniform.  Issues run two steps ahead and, past the last tile,
+    // read groups beyond the rows (zeros past the end), never computed.
+    int ki = 0, si = 0, kc = 0, sc = 0;
+    auto issue_next = [&](MbBuf<MB>& buf) {
+        mb_issue<MB, H>(buf, rs, rb + (int64_t)si * R, ki, ng, lane);
+        if (++si == steps) si = 0, ++ki;
+    };
+    auto compute_next = [&](const MbBuf<MB>& buf) {
+        mb_compute<MB, H>(buf, xr, part, sc * R, nrow - sc * R, lane);
+        if (++sc == steps) {
+            sc = 0;
+            if (++kc < ntiles) load_x(kc);
         }
+    };
+    // Starts two steps early so that the first pass only issues and every
+    // load comes from the same two issue sites.
+    MbBuf<MB> a, b;
+    for (int t = -2; t < total; t += 2) {
+        if (t >= 0) compute_next(a);
+        issue_next(a);
+        if (t + 1 >= 0 && t + 1 < total) compute_next(b);
+        issue_next(b);
     }
     wave_lds_sync();
     for (int i = lane; i < nrow * MB; i += kWave) {
@@ -246,6 +294,16 @@ __device__ __forceinline__ void mb_range(const void* packed, const uint16_t* sca
         if (mi < m) gbl(y)[mi * n + rb + r] = __half_as_ushort(__float2half_rn(part[i]));
     }
     wave_lds_sync();  // the slice is free again
+}
+
+// Two row sets of 32-group tiles when that pads a row's groups less than
+// 64-group tiles do (96 groups: three full tiles instead of one and a half).
+template <int MB>
+__device__ __forceinline__ void mb_range_any(const void* packed, const uint16_t* scales, const uint16_t* x,
+                                             uint16_t* y, int64_t n, int ng, int m, int64_t rb, int64_t re,
+                                             float* part, int lane) {
+    if (mb_two_sets(ng)) mb_range<MB, 2>(packed, scales, x, y, n, ng, m, rb, re, part, lane);
+    else mb_range<MB, 1>(packed, scales, x, y, n, ng, m, rb, re, part, lane);
 }
 
 template <int MB>
@@ -257,7 +315,8 @@ __global__ __launch_bounds__(kBlock) void gemv_mb_kernel(const void* packed, con
     const int64_t rb = wave * rows_per_wave;
     if (rb >= n) return;
     __shared__ float s_part[kWavesPerBlock][kMbRows * MB];
-    mb_range<MB>(packed, scales, x, y, n, ng, m, rb, min(n, rb + rows_per_wave), s_part[threadIdx.x / kWave], lane);
+    mb_range_any<MB>(packed, scales, x, y, n, ng, m, rb, min(n, rb + rows_per_wave), s_part[threadIdx.x / kWave],
+                     lane);
 }
 
 // Independent linears of a decode step in one launch: entry i owns waves
@@ -279,16 +338,16 @@ __global__ __launch_bounds__(kBlock) void grouped_mb_kernel(const DecodeEntry* _
     const int64_t rb = (wave - e.first_step) * e.pad;
     const int64_t k = (int64_t)e.ng * kGroup;
     __shared__ float s_part[kWavesPerBlock][kMbRows * MB];
-    mb_range<MB>(e.packed, e.scales, e.x + m0 * k, e.y + m0 * e.n, e.n, e.ng, m, rb, min(e.n, rb + e.pad),
+    mb_range_any<MB>(e.packed, e.scales, e.x + m0 * k, e.y + m0 * e.n, e.n, e.ng, m, rb, min(e.n, rb + e.pad),
                  s_part[threadIdx.x / kWave], lane);
 }
 
 template <int MB>
 hipError_t launch_mb(const uint32_t* packed, const uint16_t* scales, const uint16_t* x, uint16_t* y, int64_t n,
                      int64_t ng, int m, hipStream_t stream) {
-    const int64_t steps = (n + kMbU - 1) / kMbU;
-    const int64_t spw = min((steps + kTargetWaves - 1) / kTargetWaves, (int64_t)(kMbRows / kMbU));
-    const int64_t rows_per_wave = spw * kMbU;
+    const int64_t steps = (n + kMbStep - 1) / kMbStep;
+    const int64_t spw = min((steps + kTargetWaves - 1) / kTargetWaves, (int64_t)(kMbRows / kMbStep));
+    const int64_t rows_per_wave = spw * kMbStep;
     const int64_t waves = (n + rows_per_wave - 1) / rows_per_wave;
     const int64_t blocks = (waves + kWavesPerBlock - 1) / kWavesPerBlock;
     hipLaunchKernelGGL((gemv_mb_kernel<MB>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, packed, scales, x, y,
@@ -373,10 +432,27 @@ hipError_t launch_grouped_mb(const DecodeEntry* entries, int count, int64_t wave
     return hipGetLastError();
 }
 
-int mb_rows_per_wave(int64_t total_rows) {
-    // About 2048 waves over the whole launch, at most kMbRows rows each.
-    const int64_t r = (total_rows + kTargetWaves - 1) / kTargetWaves;
-    return (int)min((int64_t)kMbRows, max((int64_t)kMbU, (r + kMbU - 1) / kMbU * kMbU));
+hipError_t mb_target_waves(int m, int device, int64_t& waves) {
+    int per_cu = 0, cus = 0;
+    hipError_t e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device);
+    if (e != hipSuccess) return e;
+    if (m <= 2) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, grouped_mb_kernel<2>, kBlock, 0);
+    else if (m <= 4) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, grouped_mb_kernel<4>, kBlock, 0);
+    else e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, grouped_mb_kernel<8>, kBlock, 0);
+    if (e != hipSuccess) return e;
+    cus = cus > 0 ? cus : 1;
+    // Several rounds of waves, not one: with every wave resident at once the
+    // CUs that happen to hold more of them set the time, while later rounds
+    // go to whichever CU frees up first.  32 per CU measured best or within
+    // noise of it on the 3B and 8B decode steps (M = 2, 4, 7).
+    waves = max((int64_t)(per_cu > 0 ? per_cu : 1) * cus * kWavesPerBlock, (int64_t)32 * cus);
+    return hipSuccess;
+}
+
+int mb_rows_for_work(int64_t work, int64_t ng) {
+    const int64_t ngp = mb_padded_groups(ng);
+    const int64_t r = (work + ngp - 1) / ngp;
+    return (int)min((int64_t)kMbRows, max((int64_t)kMbStep, (r + kMbStep - 1) / kMbStep * kMbStep));
 }
 
 bool vector_small_batch() {

@@ -286,6 +286,25 @@ def test_small_batch_independent_linears_bit_exact(m):
         check_exact(lin[3], oracle.gemv(p, s, x, n, k), f"M={m} {n}x{k}")
 
 
+@pytest.mark.parametrize("m", [2, 3, 5])
+def test_small_batch_3b_layer_bit_exact(m):
+    """The 3B layer's four linears (96-group rows walked in 32-group tiles,
+    and the 256-group down projection) in one grouped vector launch; every
+    row checked."""
+    rng = np.random.default_rng(500 + m)
+    shapes = [(lin.n, lin.k) for lin in wl.LLAMA3B_LAYER]
+    announce(f"decode small batch M={m}, 3B layer")
+    host, lins = [], []
+    for n, k in shapes:
+        p, s = int_linear(rng, n, k, 1 / 4)
+        x = rng.integers(-1, 2, size=(m, k)).astype(np.float16)
+        host.append((p, s, x))
+        lins.append((to_dev(p), to_dev(s), to_dev(x), nan_out(m, n)))
+    run(lins, m=m)
+    for (p, s, x), lin, (n, k) in zip(host, lins, shapes):
+        check_exact(lin[3], oracle.gemv(p, s, x, n, k), f"M={m} {n}x{k}")
+
+
 @pytest.mark.parametrize("m", [4, 16])
 def test_small_batch_dependency_chain_bit_exact(m):
     """x of linear i+1 is y of linear i for 12 linears: every linear is its

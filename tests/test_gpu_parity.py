@@ -180,6 +180,29 @@ def test_gemv_integer_exact_small_batch(n, k, m):
     _gemv_case(p, s, x, sample_rows(n, 256, 11), True, "integer-exact")
 
 
+# Group counts that the vector small-batch kernel walks in 32-group tiles
+# with two row sets per wave (96 and 160 groups: an odd multiple of 32; 1, 2,
+# 31 and 32 groups: below one 64-group tile), and the 3B layer's widths.
+SHAPES_32_GROUP_TILES = SHAPES_3B + [(1, 32), (3, 64), (33, 992), (8, 1024), (1000, 5120)]
+
+
+@pytest.mark.parametrize("n,k", SHAPES_32_GROUP_TILES, ids=lambda v: str(v))
+@pytest.mark.parametrize("m", [2, 3, 4, 7])
+def test_gemv_integer_exact_small_batch_32_group_tiles(n, k, m):
+    p = wl.random_words_host(5 * n + k + m, n, k)
+    s = wl.constant_scales_host(n, k, 0x2400)
+    x = wl.small_int_x_host(n + 7 * k + m, m, k)
+    _gemv_case(p, s, x, sample_rows(n, 256, 19), True, "integer-exact")
+
+
+def test_gemv_integer_exact_small_batch_3b_lm_head():
+    n, k = wl.LLAMA3B_LM_HEAD.n, wl.LLAMA3B_LM_HEAD.k
+    p = wl.random_words_host(23, n, k)
+    s = wl.constant_scales_host(n, k, 0x2400)
+    x = wl.small_int_x_host(29, 4, k)
+    _gemv_case(p, s, x, sample_rows(n, 512, 31), True, "integer-exact LM head")
+
+
 @pytest.mark.parametrize("n,k", SHAPES_3B + SHAPES_8B + SHAPES_TP + SHAPES_EDGE, ids=lambda v: str(v))
 def test_gemv_random_weights_tolerance_m1(n, k):
     w = wl.weights_host(1000 + n + k, n, k)
