@@ -125,7 +125,7 @@ __global__ __launch_bounds__(kBlock) void gemv_m1_kernel(const u32x4* packed, co
 // once to fp16.
 constexpr int kMbRows = 256;
 constexpr int kMbU = 4;
-constexpr int kMbStep = 2 * kMbU;  // rows per wave are a multiple of a step of either tiling
+constexpr int kMbStep = 2 * kMbU;  // grouped plans: rows per wave are a multiple of a step of either tiling
 
 template <int MB>
 struct MbBuf {
@@ -345,9 +345,12 @@ __global__ __launch_bounds__(kBlock) void grouped_mb_kernel(const DecodeEntry* _
 template <int MB>
 hipError_t launch_mb(const uint32_t* packed, const uint16_t* scales, const uint16_t* x, uint16_t* y, int64_t n,
                      int64_t ng, int m, hipStream_t stream) {
-    const int64_t steps = (n + kMbStep - 1) / kMbStep;
-    const int64_t spw = min((steps + kTargetWaves - 1) / kTargetWaves, (int64_t)(kMbRows / kMbStep));
-    const int64_t rows_per_wave = spw * kMbStep;
+    // Rows per wave in whole steps of the row's tiling (4 rows with 64-group
+    // tiles, 8 with two row sets), about kTargetWaves waves.
+    const int64_t r = mb_two_sets(ng) ? 2 * kMbU : kMbU;
+    const int64_t steps = (n + r - 1) / r;
+    const int64_t spw = min((steps + kTargetWaves - 1) / kTargetWaves, (int64_t)kMbRows / r);
+    const int64_t rows_per_wave = spw * r;
     const int64_t waves = (n + rows_per_wave - 1) / rows_per_wave;
     const int64_t blocks = (waves + kWavesPerBlock - 1) / kWavesPerBlock;
     hipLaunchKernelGGL((gemv_mb_kernel<MB>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, packed, scales, x, y,
