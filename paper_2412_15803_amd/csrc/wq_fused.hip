@@ -39,7 +39,6 @@ constexpr int kBlock = 256;
 constexpr int kWavesPerBlock = kBlock / kWave;
 constexpr int kTargetWaves = 256 * 8;
 constexpr int kMaxK = (int)WQ_FUSED_MAX_K;
-constexpr int kChunksPerThread = kMaxK / 8 / kBlock;  // 8-element chunks of x per thread
 constexpr int kArgThreads = 1024;
 
 struct Args {
@@ -78,28 +77,34 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
     return t;
 }
 
-// x_eff of the whole row into LDS (all threads of the block take part).
-__device__ __forceinline__ void stage_prologue(const Args& a, uint16_t* s_x, float* red) {
+// x_eff of the whole row into LDS (all threads of the block take part): one
+// round trip for x and the second operand (norm weight or up half), then
+// `between()` (loads the caller wants in flight behind these), then the
+// arithmetic, the LDS writes and a barrier.  CPT 8-element chunks of x per
+// thread cover rows of up to 256 CPT groups.
+template <int CPT, typename F>
+__device__ __forceinline__ void stage_prologue(const Args& a, uint16_t* s_x, float* red, F between) {
     const int tid = threadIdx.x;
     const int chunks = a.ng * (kGroup / 8);
     const WQ_GLOBAL u32x4* xs = gbl(reinterpret_cast<const u32x4*>(a.x));
     const WQ_GLOBAL u32x4* bs = a.prologue == WQ_PROLOGUE_RMSNORM
                                     ? gbl(reinterpret_cast<const u32x4*>(a.norm))
                                     : gbl(reinterpret_cast<const u32x4*>(a.x)) + chunks;  // the up half
-    u32x4 xa[kChunksPerThread], xb[kChunksPerThread];
+    u32x4 xa[CPT], xb[CPT];
 #pragma unroll
-    for (int r = 0; r < kChunksPerThread; ++r) {
+    for (int r = 0; r < CPT; ++r) {
         const int c = tid + r * kBlock;
         if (c < chunks) {
             xa[r] = xs[c];
             xb[r] = bs[c];
         }
     }
+    between();
     float inv = 0.0f;
     if (a.prologue == WQ_PROLOGUE_RMSNORM) {
         float ss = 0.0f;
 #pragma unroll
-        for (int r = 0; r < kChunksPerThread; ++r) {
+        for (int r = 0; r < CPT; ++r) {
             if (tid + r * kBlock >= chunks) continue;
             const uint32_t w[4] = {xa[r].x, xa[r].y, xa[r].z, xa[r].w};
 #pragma unroll
@@ -113,7 +118,7 @@ __device__ __forceinline__ void stage_prologue(const Args& a, uint16_t* s_x, flo
         inv = 1.0f / sqrtf(total / (float)(a.ng * kGroup) + a.eps);
     }
 #pragma unroll
-    for (int r = 0; r < kChunksPerThread; ++r) {
+    for (int r = 0; r < CPT; ++r) {
         const int c = tid + r * kBlock;
         if (c >= chunks) continue;
         const uint32_t wa[4] = {xa[r].x, xa[r].y, xa[r].z, xa[r].w};
@@ -133,6 +138,37 @@ __device__ __forceinline__ void stage_prologue(const Args& a, uint16_t* s_x, flo
         reinterpret_cast<u32x4*>(s_x)[c] = u32x4{o[0], o[1], o[2], o[3]};
     }
     __syncthreads();
+}
+
+// load_x_lane in two halves, so that other loads can be issued between them
+// without waiting: the raw loads of this lane's groups, then their pairing
+// (lanes whose group index runs past the row get zeros).
+template <int LPR, int GPL>
+__device__ __forceinline__ void x_lane_raw(const uint16_t* x, int ng, int lane, u32x4 (&raw)[GPL][4]) {
+    const int sub = lane & (LPR - 1);
+#pragma unroll
+    for (int j = 0; j < GPL; ++j) {
+        const WQ_GLOBAL u32x4* src = gbl(reinterpret_cast<const u32x4*>(x + (int64_t)min(sub + LPR * j, ng - 1) * kGroup));
+#pragma unroll
+        for (int c = 0; c < 4; ++c) raw[j][c] = src[c];
+    }
+}
+
+template <int LPR, int GPL>
+__device__ __forceinline__ void x_lane_pair(const u32x4 (&raw)[GPL][4], int ng, int lane, half2v (&xr)[GPL][16]) {
+    const int sub = lane & (LPR - 1);
+#pragma unroll
+    for (int j = 0; j < GPL; ++j) {
+        const bool act = sub + LPR * j < ng;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const u32x4 d = raw[j][c];
+            xr[j][4 * c + 0] = as_h2(act ? (d.x & 0xFFFFu) | (d.z << 16) : 0u);
+            xr[j][4 * c + 1] = as_h2(act ? (d.x >> 16) | (d.z & 0xFFFF0000u) : 0u);
+            xr[j][4 * c + 2] = as_h2(act ? (d.y & 0xFFFFu) | (d.w << 16) : 0u);
+            xr[j][4 * c + 3] = as_h2(act ? (d.y >> 16) | (d.w & 0xFFFF0000u) : 0u);
+        }
+    }
 }
 
 // load_x_lane with x_eff already in LDS.
@@ -196,33 +232,74 @@ __global__ __launch_bounds__(kBlock) void fused_m1_kernel(const Args a) {
     __shared__ float s_red[kWavesPerBlock];
     const int lane = threadIdx.x & (kWave - 1);
 
-    half2v xr[GPL][16];
-    if (a.prologue != WQ_PROLOGUE_NONE) {
-        stage_prologue(a, s_x, s_red);
-        load_x_lane_lds<LPR, GPL>(s_x, a.ng, lane, xr);
-    } else {
-        load_x_lane<LPR, GPL, GPL>(a.x, a.ng, lane, xr);
-    }
-
     const int64_t wave = (int64_t)__builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerBlock + threadIdx.x / kWave);
     const int64_t rb = wave * a.rows_per_wave;
-    if (rb >= a.n) return;
     const int64_t re = min(a.n, rb + a.rows_per_wave);
-    const int64_t steps = (re - rb + R - 1) / R;
-    const LinearRsrc rs = make_rsrc(a.packed, a.scales, (uint32_t)(a.n * a.ng * 2));
     float* ylds = s_y[threadIdx.x / kWave];
-
-    // As in gemv_m1_kernel: unconditional issues from two sites, so the wait
-    // counts stay exact; past the matrix the loads read zeros.
+    half2v xr[GPL][16];
     StepBuf b0, b1;
-    for (int64_t s = -2; s < steps; s += 2) {
-        const int64_t ra = rb + s * R;
-        if (s >= 0) compute_step_f32<LPR, GPL>(b0, xr, (int)min((int64_t)R, re - ra), ylds, (int)(s * R), lane);
-        issue_step<LPR, GPL>(b0, rs, ra + 2 * R, a.ng, lane);
-        const int64_t rbb = ra + R;
-        if (s + 1 >= 0 && s + 1 < steps)
-            compute_step_f32<LPR, GPL>(b1, xr, (int)min((int64_t)R, re - rbb), ylds, (int)((s + 1) * R), lane);
-        issue_step<LPR, GPL>(b1, rs, rbb + 2 * R, a.ng, lane);
+    if constexpr (LPR * GPL <= 256) {
+        // x (and the prologue's second operand) is loaded first and the first
+        // two weight steps right after it: the weights are then in flight
+        // while x is rearranged and the prologue computed, and waiting for x
+        // never waits for them (the load counter retires in issue order).
+        // Waves past the matrix take part in the prologue's barriers; their
+        // loads read zeros.
+        const int64_t steps = rb < a.n ? (re - rb + R - 1) / R : 0;
+        const LinearRsrc rs = make_rsrc(a.packed, a.scales, (uint32_t)(a.n * a.ng * 2));
+        if (a.prologue != WQ_PROLOGUE_NONE) {
+            // 8-element chunks of x per thread for the longest row of this
+            // shape (LPR GPL groups: the launcher picks a shape covering the
+            // row), not of the largest K, to keep registers free for the
+            // weight loads issued beside them.
+            constexpr int CPT = (LPR * GPL * kGroup / 8 + kBlock - 1) / kBlock;
+            stage_prologue<CPT>(a, s_x, s_red, [&] {
+                issue_step<LPR, GPL>(b0, rs, rb, a.ng, lane);
+                issue_step<LPR, GPL>(b1, rs, rb + R, a.ng, lane);
+            });
+            load_x_lane_lds<LPR, GPL>(s_x, a.ng, lane, xr);
+        } else {
+            u32x4 raw[GPL][4];
+            x_lane_raw<LPR, GPL>(a.x, a.ng, lane, raw);
+            issue_step<LPR, GPL>(b0, rs, rb, a.ng, lane);
+            issue_step<LPR, GPL>(b1, rs, rb + R, a.ng, lane);
+            x_lane_pair<LPR, GPL>(raw, a.ng, lane, xr);
+        }
+        if (rb >= a.n) return;
+        // As in gemv_m1_kernel: unconditional issues (past the matrix the
+        // loads read zeros), so the wait counts stay exact.
+        for (int64_t s = 0; s < steps; s += 2) {
+            const int64_t ra = rb + s * R;
+            compute_step_f32<LPR, GPL>(b0, xr, (int)min((int64_t)R, re - ra), ylds, (int)(s * R), lane);
+            issue_step<LPR, GPL>(b0, rs, ra + 2 * R, a.ng, lane);
+            const int64_t rbb = ra + R;
+            if (s + 1 < steps)
+                compute_step_f32<LPR, GPL>(b1, xr, (int)min((int64_t)R, re - rbb), ylds, (int)((s + 1) * R), lane);
+            issue_step<LPR, GPL>(b1, rs, rbb + 2 * R, a.ng, lane);
+        }
+    } else {
+        // Rows of more than 256 groups: x first, then the weights (their x
+        // and weight registers together would cost waves per SIMD).  The
+        // loop starts two steps early so that the first pass only issues and
+        // every load comes from the same two issue sites.
+        if (a.prologue != WQ_PROLOGUE_NONE) {
+            stage_prologue<kMaxK / 8 / kBlock>(a, s_x, s_red, [] {});
+            load_x_lane_lds<LPR, GPL>(s_x, a.ng, lane, xr);
+        } else {
+            load_x_lane<LPR, GPL, GPL>(a.x, a.ng, lane, xr);
+        }
+        if (rb >= a.n) return;
+        const int64_t steps = (re - rb + R - 1) / R;
+        const LinearRsrc rs = make_rsrc(a.packed, a.scales, (uint32_t)(a.n * a.ng * 2));
+        for (int64_t s = -2; s < steps; s += 2) {
+            const int64_t ra = rb + s * R;
+            if (s >= 0) compute_step_f32<LPR, GPL>(b0, xr, (int)min((int64_t)R, re - ra), ylds, (int)(s * R), lane);
+            issue_step<LPR, GPL>(b0, rs, ra + 2 * R, a.ng, lane);
+            const int64_t rbb = ra + R;
+            if (s + 1 >= 0 && s + 1 < steps)
+                compute_step_f32<LPR, GPL>(b1, xr, (int)min((int64_t)R, re - rbb), ylds, (int)((s + 1) * R), lane);
+            issue_step<LPR, GPL>(b1, rs, rbb + 2 * R, a.ng, lane);
+        }
     }
     flush_y_residual(a.y, a.residual, rb, ylds, (int)(re - rb), lane);
 }
