@@ -62,7 +62,7 @@ __device__ __forceinline__ void transpose4(uint32_t& a0, uint32_t& a1, uint32_t&
     a2 = q23[0]; a3 = q23[1];
 }
 
-constexpr int kChunk = 4;   // steps of 4 groups whose x a wave holds at once
+constexpr int kChunk = 4;   // steps of 4 groups whose x a wave holds at once (2 in some single-linear launches)
 constexpr int kDepth = 8;   // items in flight per wave
 
 // Issue item (tile tt, step s): rows row0 + 16 tt + (lane % 16), group
@@ -125,14 +125,14 @@ __device__ __forceinline__ void load_x_step(const uint16_t* xrow, int s, int ng,
 
 // A block owns T tiles of 16 weight rows from row0 of one linear; its waves
 // (blockDim / 64 of them) split the row's steps into contiguous ranges.  A
-// wave takes its range in chunks of kChunk steps: it loads the chunk's x
+// wave takes its range in chunks of C steps: it loads the chunk's x
 // once, then streams every tile's codes for those steps through a
 // kDepth-item register pipeline.  The waves' partial tiles are summed through
 // LDS in a fixed order and one wave per tile rounds and stores it.
-template <int T>
+template <int T, int C = kChunk>
 __device__ __forceinline__ void mfma_block(const void* packed, const uint16_t* scales, const uint16_t* x,
                                            uint16_t* y, int64_t n, int ng, int m, int64_t row0) {
-    constexpr int kItems = T * kChunk;
+    constexpr int kItems = T * C;
     constexpr int kPre = kDepth < kItems ? kDepth : kItems;
     const int lane = threadIdx.x & (kWave - 1);
     const int nw = blockDim.x / kWave;
@@ -148,19 +148,19 @@ __device__ __forceinline__ void mfma_block(const void* packed, const uint16_t* s
 #pragma unroll
     for (int tt = 0; tt < T; ++tt) acc[tt] = float4v{0.0f, 0.0f, 0.0f, 0.0f};
 
-    for (int c0 = sb; c0 < se; c0 += kChunk) {
+    for (int c0 = sb; c0 < se; c0 += C) {
         MItem buf[kPre];
 #pragma unroll
-        for (int q = 0; q < kPre; ++q) issue_item(buf[q], rs, lg, row0, q / kChunk, c0 + q % kChunk, ng);
-        half8 xa[kChunk][4];
+        for (int q = 0; q < kPre; ++q) issue_item(buf[q], rs, lg, row0, q / C, c0 + q % C, ng);
+        half8 xa[C][4];
 #pragma unroll
-        for (int k = 0; k < kChunk; ++k) load_x_step(xrow, min(c0 + k, nsteps - 1), ng, c, xa[k]);
+        for (int k = 0; k < C; ++k) load_x_step(xrow, min(c0 + k, nsteps - 1), ng, c, xa[k]);
 #pragma unroll
         for (int q = 0; q < kItems; ++q) {
-            const int tt = q / kChunk, k = q % kChunk, s = c0 + k;
+            const int tt = q / C, k = q % C, s = c0 + k;
             compute_item(buf[q % kPre], xa[k], acc[tt], s < se && 4 * s + c < ng);
             if (q + kPre < kItems)
-                issue_item(buf[q % kPre], rs, lg, row0, (q + kPre) / kChunk, c0 + (q + kPre) % kChunk, ng);
+                issue_item(buf[q % kPre], rs, lg, row0, (q + kPre) / C, c0 + (q + kPre) % C, ng);
         }
     }
 
@@ -197,11 +197,11 @@ __device__ __forceinline__ void mfma_block(const void* packed, const uint16_t* s
 }
 
 // One linear: block b owns rows [16 T b, 16 T (b + 1)).
-template <int T>
+template <int T, int C>
 __global__ __launch_bounds__(512) void gemm_mfma_kernel(const void* packed, const uint16_t* scales,
                                                         const uint16_t* __restrict__ x, uint16_t* __restrict__ y,
                                                         int64_t n, int ng, int m) {
-    mfma_block<T>(packed, scales, x, y, n, ng, m, (int64_t)blockIdx.x * 16 * T);
+    mfma_block<T, C>(packed, scales, x, y, n, ng, m, (int64_t)blockIdx.x * 16 * T);
 }
 
 // Independent linears of a decode step in one launch: entry i owns blocks
@@ -223,12 +223,12 @@ __global__ __launch_bounds__(512) void grouped_mfma_kernel(const DecodeEntry* __
                   (b - e.first_step) * 16 * T);
 }
 
-template <int T>
+template <int T, int C>
 hipError_t launch_t(const uint32_t* packed, const uint16_t* scales, const uint16_t* x, uint16_t* y, int64_t n,
                     int64_t ng, int m, int w, hipStream_t stream) {
     const int64_t blocks = (n + 16 * T - 1) / (16 * T);
-    hipLaunchKernelGGL((gemm_mfma_kernel<T>), dim3((unsigned)blocks), dim3(64 * w), 0, stream, packed, scales, x, y,
-                       n, (int)ng, m);
+    hipLaunchKernelGGL((gemm_mfma_kernel<T, C>), dim3((unsigned)blocks), dim3(64 * w), 0, stream, packed, scales, x,
+                       y, n, (int)ng, m);
     return hipGetLastError();
 }
 
@@ -247,8 +247,13 @@ hipError_t launch_gemm_mfma(const uint32_t* packed, const uint16_t* scales, cons
                             int64_t n, int64_t k, int64_t m, hipStream_t stream) {
     const int64_t ng = k / kGroup;
     const int64_t nsteps = (ng + 3) / 4;
+    // Chunks of 2 steps (half the x registers, twice the waves per SIMD) for
+    // the very tall and the very long linears, where that measured faster
+    // (LM heads and K = 14336 at M = 8 and 16: about 12%); 4 elsewhere
+    // (3B qkv and gate_up, 8B gate_up: 3-14% slower with 2).
+    const int c = (n >= 65536 || ng >= 384) ? 2 : kChunk;
     // Waves per block: one chunk of steps each where K allows, at most 8.
-    const int w = (int)std::min<int64_t>(8, (nsteps + kChunk - 1) / kChunk);
+    const int w = (int)std::min<int64_t>(8, (nsteps + c - 1) / c);
     // Tiles per block: as many (up to 8, sharing each x load) as still keep
     // about 1536 waves in flight.
     int t = 8;
@@ -258,11 +263,15 @@ hipError_t launch_gemm_mfma(const uint32_t* packed, const uint16_t* scales, cons
         const uint16_t* xc = x + m0 * k;
         uint16_t* yc = y + m0 * n;
         hipError_t e = hipSuccess;
-        switch (t) {
-            case 8: e = launch_t<8>(packed, scales, xc, yc, n, ng, mc, w, stream); break;
-            case 4: e = launch_t<4>(packed, scales, xc, yc, n, ng, mc, w, stream); break;
-            case 2: e = launch_t<2>(packed, scales, xc, yc, n, ng, mc, w, stream); break;
-            default: e = launch_t<1>(packed, scales, xc, yc, n, ng, mc, w, stream); break;
+        switch (t * 10 + c) {
+            case 84: e = launch_t<8, 4>(packed, scales, xc, yc, n, ng, mc, w, stream); break;
+            case 44: e = launch_t<4, 4>(packed, scales, xc, yc, n, ng, mc, w, stream); break;
+            case 24: e = launch_t<2, 4>(packed, scales, xc, yc, n, ng, mc, w, stream); break;
+            case 14: e = launch_t<1, 4>(packed, scales, xc, yc, n, ng, mc, w, stream); break;
+            case 82: e = launch_t<8, 2>(packed, scales, xc, yc, n, ng, mc, w, stream); break;
+            case 42: e = launch_t<4, 2>(packed, scales, xc, yc, n, ng, mc, w, stream); break;
+            case 22: e = launch_t<2, 2>(packed, scales, xc, yc, n, ng, mc, w, stream); break;
+            default: e = launch_t<1, 2>(packed, scales, xc, yc, n, ng, mc, w, stream); break;
         }
         if (e != hipSuccess) return e;
     }

@@ -195,11 +195,14 @@ def test_gemv_integer_exact_small_batch_32_group_tiles(n, k, m):
     _gemv_case(p, s, x, sample_rows(n, 256, 19), True, "integer-exact")
 
 
-def test_gemv_integer_exact_small_batch_3b_lm_head():
+@pytest.mark.parametrize("m", [4, 16])
+def test_gemv_integer_exact_small_batch_3b_lm_head(m):
+    """The 3B LM head on the vector kernel (M=4) and on the matrix cores with
+    2-step chunks (M=16, the launch used for very tall linears)."""
     n, k = wl.LLAMA3B_LM_HEAD.n, wl.LLAMA3B_LM_HEAD.k
     p = wl.random_words_host(23, n, k)
     s = wl.constant_scales_host(n, k, 0x2400)
-    x = wl.small_int_x_host(29, 4, k)
+    x = wl.small_int_x_host(29 + m, m, k)
     _gemv_case(p, s, x, sample_rows(n, 512, 31), True, "integer-exact LM head")
 
 
