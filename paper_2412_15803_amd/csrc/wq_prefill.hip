@@ -58,7 +58,7 @@ __device__ __forceinline__ u32x4 to_dequant_order(const u32x4 d) {
     return r;
 }
 
-__global__ __launch_bounds__(kThreads) void prefill_kernel(const u32x4* __restrict__ packed,
+__global__ __launch_bounds__(kThreads, 2) void prefill_kernel(const u32x4* __restrict__ packed,
                                                            const uint16_t* __restrict__ scales,
                                                            const uint16_t* __restrict__ x, uint16_t* __restrict__ y,
                                                            int m, int n, int k, int blocks_m) {
@@ -73,36 +73,50 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(const u32x4* __restri
     const int ng = k / kGroup;
     const int stages = (k + kBK - 1) / kBK;
 
-    // This thread's share of a stage's global loads.
-    u32x4 ra[4];
-    u32x4 rb;
-    uint32_t rs;
+    // This thread's share of a stage's global loads, in two register sets:
+    // the loads of stage s + 2 are issued while stage s is multiplied and
+    // stage s + 1 is written to LDS.  All loads are buffer loads whose offset
+    // is set past the buffer for pieces outside the matrices (they read
+    // zeros: x = 0, codes 0 with scale 0 give weight 0), so there is no
+    // branch around a load and the waits stay exact.
+    struct Regs {
+        u32x4 a[4];
+        u32x4 b;
+        uint32_t s;
+    };
+    constexpr uint32_t kOut = 0xFFFFFFF0u;
+    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(x), (short)0, (int)((uint32_t)m * (uint32_t)k * 2u), kRawBufferFlags);
+    const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<u32x4*>(packed), (short)0, (int)((uint32_t)n * (uint32_t)ng * 16u), kRawBufferFlags);
+    const __amdgpu_buffer_rsrc_t sr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(scales), (short)0, (int)((uint32_t)n * (uint32_t)ng * 2u), kRawBufferFlags);
     const int bn = tid >> 1, bgrp = tid & 1;  // weight row and group (of two) of the B piece
-    auto load_stage = [&](int s) {
+    auto load_stage = [&](int s, Regs& R) {
         const int k0 = s * kBK;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int c = tid + kThreads * i;
             const int row = c >> 3, kc = c & 7;
             const int gm = m0 + row, gk = k0 + 8 * kc;
-            ra[i] = (gm < m && gk < k)
-                        ? *reinterpret_cast<const WQ_GLOBAL u32x4*>(gbl(x) + (int64_t)gm * k + gk)
-                        : u32x4{0u, 0u, 0u, 0u};
+            const uint32_t off = (gm < m && gk < k) ? ((uint32_t)gm * (uint32_t)k + (uint32_t)gk) * 2u : kOut;
+            R.a[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0));
         }
         const int gn = n0 + bn, g = 2 * s + bgrp;
         const bool ok = gn < n && g < ng;
-        rb = ok ? gbl(packed)[(int64_t)gn * ng + g] : u32x4{0x88888888u, 0x88888888u, 0x88888888u, 0x88888888u};
-        rs = ok ? (uint32_t)gbl(scales)[(int64_t)gn * ng + g] : 0u;
+        const uint32_t gi = (uint32_t)gn * (uint32_t)ng + (uint32_t)g;
+        R.b = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(wr, ok ? gi * 16u : kOut, 0, 0));
+        R.s = __builtin_amdgcn_raw_buffer_load_b16(sr, ok ? gi * 2u : kOut, 0, 0);
     };
-    auto store_stage = [&](Stage& S) {
+    auto store_stage = [&](Stage& S, const Regs& R) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int c = tid + kThreads * i;
             const int row = c >> 3, kc = c & 7;
-            *reinterpret_cast<u32x4*>(&S.a[row][8 * kc]) = to_dequant_order(ra[i]);
+            *reinterpret_cast<u32x4*>(&S.a[row][8 * kc]) = to_dequant_order(R.a[i]);
         }
-        const half2v sc = as_h2(rs | (rs << 16));
-        const uint32_t w[4] = {rb.x, rb.y, rb.z, rb.w};
+        const half2v sc = as_h2(R.s | (R.s << 16));
+        const uint32_t w[4] = {R.b.x, R.b.y, R.b.z, R.b.w};
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             half2v q[4];
@@ -120,13 +134,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(const u32x4* __restri
         for (int j = 0; j < 4; ++j) acc[i][j] = float4v{0.0f, 0.0f, 0.0f, 0.0f};
 
     const int r = lane & 15, c = lane >> 4;
-    load_stage(0);
-    store_stage(st[0]);
-    __syncthreads();
-    for (int s = 0; s < stages; ++s) {
-        const bool more = s + 1 < stages;
-        if (more) load_stage(s + 1);
-        const Stage& S = st[s & 1];
+    auto compute = [&](const Stage& S) {
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
             half8 fa[4], fb[4];
@@ -142,7 +150,25 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(const u32x4* __restri
                 for (int j = 0; j < 4; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fa[i], fb[j], acc[i][j], 0, 0, 0);
         }
-        if (more) store_stage(st[(s + 1) & 1]);
+    };
+
+    // Stages in pairs: LDS buffer and register set s & 1.  Loads past the
+    // last stage read zeros and are never stored.
+    Regs R0, R1;
+    load_stage(0, R0);
+    load_stage(1, R1);
+    store_stage(st[0], R0);
+    load_stage(2, R0);
+    __syncthreads();
+    for (int s = 0; s < stages; s += 2) {
+        compute(st[0]);
+        store_stage(st[1], R1);  // stage s + 1
+        load_stage(s + 3, R1);
+        __syncthreads();
+        if (s + 1 == stages) break;
+        compute(st[1]);
+        store_stage(st[0], R0);  // stage s + 2
+        load_stage(s + 4, R0);
         __syncthreads();
     }
 
