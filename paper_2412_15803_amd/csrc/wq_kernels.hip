@@ -235,8 +235,9 @@ __device__ __forceinline__ void mb_compute(const MbBuf<MB>& b, const half2v (&xr
 // tiles form one stream through the two buffers: the loads of a tile's first
 // steps are issued while the previous tile's last steps are computed, and x
 // of the next tile is loaded right after the last step that reads the
-// current one (ahead of the next weight loads, so that waiting for x never
-// waits for those).
+// current one, ahead of the next weight loads.  Waiting for x then waits for
+// the other buffer's loads too (issued earlier, and needed next anyway), so
+// a tile boundary costs the pipeline one step of depth, not a full drain.
 template <int MB, int H>
 __device__ __forceinline__ void mb_range(const void* packed, const uint16_t* scales, const uint16_t* x, uint16_t* y,
                                          int64_t n, int ng, int m, int64_t rb, int64_t re, float* part, int lane) {
