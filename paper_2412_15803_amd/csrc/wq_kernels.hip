@@ -238,9 +238,14 @@ __device__ __forceinline__ void mb_compute(const MbBuf<MB>& b, const half2v (&xr
 // current one, ahead of the next weight loads.  Waiting for x then waits for
 // the other buffer's loads too (issued earlier, and needed next anyway), so
 // a tile boundary costs the pipeline one step of depth, not a full drain.
+//
+// Only tiles [kt0, kt1) are taken when the row's K is split across waves;
+// then the fp32 partials stay in `part` for the caller to sum, else they are
+// rounded and written to y.
 template <int MB, int H>
 __device__ __forceinline__ void mb_range(const void* packed, const uint16_t* scales, const uint16_t* x, uint16_t* y,
-                                         int64_t n, int ng, int m, int64_t rb, int64_t re, float* part, int lane) {
+                                         int64_t n, int ng, int m, int64_t rb, int64_t re, float* part, int lane,
+                                         int kt0, int kt1, bool write) {
     constexpr int T = kWave / H;
     constexpr int R = H * kMbU;
     const int nrow = (int)(re - rb);
@@ -250,8 +255,8 @@ __device__ __forceinline__ void mb_range(const void* packed, const uint16_t* sca
     for (int i = lane; i < nrow * MB; i += kWave) part[i] = 0.0f;
     wave_lds_sync();
 
-    const int ntiles = (ng + T - 1) / T;
-    const int total = ntiles * steps;
+    const int ntiles = kt1;
+    const int total = (kt1 - kt0) * steps;
     half2v xr[MB][16];
     auto load_x = [&](int kt) {
         const int g = T * kt + lane % T;
@@ -264,11 +269,11 @@ __device__ __forceinline__ void mb_range(const void* packed, const uint16_t* sca
             for (int e = 0; e < 16; ++e) xr[i][e] = act ? xr[i][e] : half2v{(_Float16)0.0f, (_Float16)0.0f};
         }
     };
-    load_x(0);
+    load_x(kt0);
     // Issue position (tile ki, step si) and compute position (kc, sc), both
     // wave-uniform.  Issues run two steps ahead and, past the last tile,
     // read groups beyond the rows (zeros past the end), never computed.
-    int ki = 0, si = 0, kc = 0, sc = 0;
+    int ki = kt0, si = 0, kc = kt0, sc = 0;
     auto issue_next = [&](MbBuf<MB>& buf) {
         mb_issue<MB, H>(buf, rs, rb + (int64_t)si * R, ki, ng, lane);
         if (++si == steps) si = 0, ++ki;
@@ -290,6 +295,7 @@ __device__ __forceinline__ void mb_range(const void* packed, const uint16_t* sca
         issue_next(b);
     }
     wave_lds_sync();
+    if (!write) return;
     for (int i = lane; i < nrow * MB; i += kWave) {
         const int r = i / MB, mi = i % MB;
         if (mi < m) gbl(y)[mi * n + rb + r] = __half_as_ushort(__float2half_rn(part[i]));
@@ -302,22 +308,48 @@ __device__ __forceinline__ void mb_range(const void* packed, const uint16_t* sca
 template <int MB>
 __device__ __forceinline__ void mb_range_any(const void* packed, const uint16_t* scales, const uint16_t* x,
                                              uint16_t* y, int64_t n, int ng, int m, int64_t rb, int64_t re,
-                                             float* part, int lane) {
-    if (mb_two_sets(ng)) mb_range<MB, 2>(packed, scales, x, y, n, ng, m, rb, re, part, lane);
-    else mb_range<MB, 1>(packed, scales, x, y, n, ng, m, rb, re, part, lane);
+                                             float* part, int lane, int split = 1, int ks = 0) {
+    if (mb_two_sets(ng)) {
+        const int nt = (ng + 31) / 32;
+        mb_range<MB, 2>(packed, scales, x, y, n, ng, m, rb, re, part, lane, ks * nt / split, (ks + 1) * nt / split,
+                        split == 1);
+    } else {
+        const int nt = (ng + 63) / 64;
+        mb_range<MB, 1>(packed, scales, x, y, n, ng, m, rb, re, part, lane, ks * nt / split, (ks + 1) * nt / split,
+                        split == 1);
+    }
 }
 
+// One linear.  With split = 1 every wave owns rows_per_wave rows; with
+// split = 2 or 4 the block's waves form 4 / split row runs, the `split`
+// waves of a run take contiguous parts of the row's K tiles, and their fp32
+// partials are summed through LDS in a fixed order before the one rounding
+// (for linears with too few rows to give every SIMD waves of its own).
 template <int MB>
 __global__ __launch_bounds__(kBlock) void gemv_mb_kernel(const void* packed, const uint16_t* scales,
                                                          const uint16_t* __restrict__ x, uint16_t* __restrict__ y,
-                                                         int64_t n, int ng, int m, int64_t rows_per_wave) {
+                                                         int64_t n, int ng, int m, int64_t rows_per_wave, int split) {
     const int lane = threadIdx.x & (kWave - 1);
-    const int64_t wave = (int64_t)__builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerBlock + threadIdx.x / kWave);
-    const int64_t rb = wave * rows_per_wave;
-    if (rb >= n) return;
+    const int wib = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int ks = wib % split;
+    const int64_t run = (int64_t)blockIdx.x * (kWavesPerBlock / split) + wib / split;
+    const int64_t rb = run * rows_per_wave;
+    const int64_t re = min(n, rb + rows_per_wave);
     __shared__ float s_part[kWavesPerBlock][kMbRows * MB];
-    mb_range_any<MB>(packed, scales, x, y, n, ng, m, rb, min(n, rb + rows_per_wave), s_part[threadIdx.x / kWave],
-                     lane);
+    if (split == 1) {
+        if (rb < n) mb_range_any<MB>(packed, scales, x, y, n, ng, m, rb, re, s_part[wib], lane);
+        return;
+    }
+    if (rb < n) mb_range_any<MB>(packed, scales, x, y, n, ng, m, rb, re, s_part[wib], lane, split, ks);
+    __syncthreads();
+    if (ks != 0 || rb >= n) return;
+    const int nrow = (int)(re - rb);
+    for (int i = lane; i < nrow * MB; i += kWave) {
+        float t = s_part[wib][i];
+        for (int j = 1; j < split; ++j) t += s_part[wib + j][i];
+        const int r = i / MB, mi = i % MB;
+        if (mi < m) gbl(y)[mi * n + rb + r] = __half_as_ushort(__float2half_rn(t));
+    }
 }
 
 // Independent linears of a decode step in one launch: entry i owns waves
@@ -340,7 +372,7 @@ __global__ __launch_bounds__(kBlock) void grouped_mb_kernel(const DecodeEntry* _
     const int64_t k = (int64_t)e.ng * kGroup;
     __shared__ float s_part[kWavesPerBlock][kMbRows * MB];
     mb_range_any<MB>(e.packed, e.scales, e.x + m0 * k, e.y + m0 * e.n, e.n, e.ng, m, rb, min(e.n, rb + e.pad),
-                 s_part[threadIdx.x / kWave], lane);
+                     s_part[threadIdx.x / kWave], lane);
 }
 
 template <int MB>
@@ -352,10 +384,15 @@ hipError_t launch_mb(const uint32_t* packed, const uint16_t* scales, const uint1
     const int64_t steps = (n + r - 1) / r;
     const int64_t spw = min((steps + kTargetWaves - 1) / kTargetWaves, (int64_t)kMbRows / r);
     const int64_t rows_per_wave = spw * r;
-    const int64_t waves = (n + rows_per_wave - 1) / rows_per_wave;
-    const int64_t blocks = (waves + kWavesPerBlock - 1) / kWavesPerBlock;
+    const int64_t runs = (n + rows_per_wave - 1) / rows_per_wave;
+    // Too few row runs to give every SIMD two waves: split each run's K
+    // tiles over 2 or 4 waves (at most one tile each).
+    const int64_t ntiles = mb_two_sets(ng) ? (ng + 31) / 32 : (ng + 63) / 64;
+    int split = 1;
+    while (split < 4 && runs * split < 2048 && ntiles >= 2 * split) split *= 2;
+    const int64_t blocks = (runs * split + kWavesPerBlock - 1) / kWavesPerBlock;
     hipLaunchKernelGGL((gemv_mb_kernel<MB>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, packed, scales, x, y,
-                       n, (int)ng, m, rows_per_wave);
+                       n, (int)ng, m, rows_per_wave, split);
     return hipGetLastError();
 }
 
