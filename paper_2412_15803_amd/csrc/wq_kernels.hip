@@ -386,7 +386,7 @@ hipError_t launch_mb(const uint32_t* packed, const uint16_t* scales, const uint1
     const int64_t rows_per_wave = spw * r;
     const int64_t runs = (n + rows_per_wave - 1) / rows_per_wave;
     // Too few row runs to give every SIMD two waves: split each run's K
-    // tiles over 2 or 4 waves (at most one tile each).
+    // tiles over 2 or 4 waves (at least one tile each).
     const int64_t ntiles = mb_two_sets(ng) ? (ng + 31) / 32 : (ng + 63) / 64;
     int split = 1;
     while (split < 4 && runs * split < 2048 && ntiles >= 2 * split) split *= 2;
