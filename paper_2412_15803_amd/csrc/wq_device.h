@@ -81,6 +81,15 @@ __device__ __forceinline__ void dequant_word(uint32_t w, half2v (&q)[4]) {
     q[3] = as_h2(and_or(w8, 0x00F000F0u, 0x64006400u)) * k1_16 + km72;
 }
 
+// a.lo b.lo + a.hi b.hi in fp32, starting a chain: the three-operand form
+// with an inline zero, where the compiler would otherwise copy a zero into
+// the accumulator and use the two-operand form.
+__device__ __forceinline__ float dot2_first(half2v a, half2v b) {
+    float r;
+    asm("v_dot2_f32_f16 %0, %1, %2, 0" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+
 __device__ __forceinline__ float dot_word(uint32_t w, const half2v* xp, float acc) {
     half2v q[4];
     dequant_word(w, q);
@@ -91,13 +100,18 @@ __device__ __forceinline__ float dot_word(uint32_t w, const half2v* xp, float ac
     return acc;
 }
 
-// sum_{k in group} (q_k - 8) * x_k for one 16-byte group of codes.
+// sum_{k in group} (q_k - 8) * x_k for one 16-byte group of codes: one
+// chain of 16 dot products, words in order.
 __device__ __forceinline__ float dot_group(const u32x4 wv, const half2v xg[16]) {
-    float a0 = dot_word(wv.x, xg + 0, 0.0f);
-    float a1 = dot_word(wv.y, xg + 4, 0.0f);
-    a0 = dot_word(wv.z, xg + 8, a0);
-    a1 = dot_word(wv.w, xg + 12, a1);
-    return a0 + a1;
+    half2v q[4];
+    dequant_word(wv.x, q);
+    float a = dot2_first(q[0], xg[0]);
+    a = __builtin_amdgcn_fdot2(q[1], xg[1], a, false);
+    a = __builtin_amdgcn_fdot2(q[2], xg[2], a, false);
+    a = __builtin_amdgcn_fdot2(q[3], xg[3], a, false);
+    a = dot_word(wv.y, xg + 4, a);
+    a = dot_word(wv.z, xg + 8, a);
+    return dot_word(wv.w, xg + 12, a);
 }
 
 template <int CTRL, int ROW_MASK>

@@ -203,8 +203,6 @@ __device__ __forceinline__ void mb_compute(const MbBuf<MB>& b, const half2v (&xr
 #pragma unroll
     for (int u = 0; u < kMbU; ++u) {
         float acc[MB];
-#pragma unroll
-        for (int i = 0; i < MB; ++i) acc[i] = 0.0f;
         const uint32_t wd[4] = {b.w[u].x, b.w[u].y, b.w[u].z, b.w[u].w};
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
@@ -213,7 +211,9 @@ __device__ __forceinline__ void mb_compute(const MbBuf<MB>& b, const half2v (&xr
 #pragma unroll
             for (int i = 0; i < MB; ++i)
 #pragma unroll
-                for (int e = 0; e < 4; ++e) acc[i] = __builtin_amdgcn_fdot2(q[e], xr[i][4 * c + e], acc[i], false);
+                for (int e = 0; e < 4; ++e)
+                    acc[i] = c == 0 && e == 0 ? dot2_first(q[0], xr[i][0])
+                                              : __builtin_amdgcn_fdot2(q[e], xr[i][4 * c + e], acc[i], false);
         }
         const float sc = __half2float(__ushort_as_half((uint16_t)b.s[u]));
 #pragma unroll
