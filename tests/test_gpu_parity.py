@@ -195,6 +195,22 @@ def test_gemv_integer_exact_small_batch_32_group_tiles(n, k, m):
     _gemv_case(p, s, x, sample_rows(n, 256, 19), True, "integer-exact")
 
 
+# Single linears with few row runs: the vector kernel splits each run's K
+# tiles over 2 or 4 waves of a block and sums their partials in LDS.  Ragged
+# N (last run of one row), uneven tile shares (5 tiles over 4 waves) and
+# several tiles per wave.
+SHAPES_K_SPLIT = [(37, 8192), (1001, 5120), (5, 16384), (3, 4096)]
+
+
+@pytest.mark.parametrize("n,k", SHAPES_K_SPLIT, ids=lambda v: str(v))
+@pytest.mark.parametrize("m", [2, 3, 5, 7])
+def test_gemv_integer_exact_small_batch_k_split(n, k, m):
+    p = wl.random_words_host(11 * n + k + m, n, k)
+    s = wl.constant_scales_host(n, k, 0x2400)
+    x = wl.small_int_x_host(3 * n + 5 * k + m, m, k)
+    _gemv_case(p, s, x, None, True, "integer-exact K split")
+
+
 @pytest.mark.parametrize("m", [4, 16])
 def test_gemv_integer_exact_small_batch_3b_lm_head(m):
     """The 3B LM head on the vector kernel (M=4) and on the matrix cores with
