@@ -211,6 +211,27 @@ def test_gemv_integer_exact_small_batch_k_split(n, k, m):
     _gemv_case(p, s, x, None, True, "integer-exact K split")
 
 
+def _random_small_batch_shapes(count, seed):
+    """Seeded (N, K, M) draws across the vector kernel's launch shapes: 64- and
+    32-group tiles, K split over 1, 2 or 4 waves, ragged row runs, M 2..7."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(count):
+        n = int(rng.choice([int(rng.integers(1, 64)), int(rng.integers(64, 1200)), int(rng.integers(1200, 6000))]))
+        k = 32 * int(rng.integers(1, 513))
+        m = int(rng.integers(2, 8))
+        out.append((n, k, m))
+    return out
+
+
+@pytest.mark.parametrize("n,k,m", _random_small_batch_shapes(24, 2024), ids=lambda v: str(v))
+def test_gemv_integer_exact_small_batch_random_shapes(n, k, m):
+    p = wl.random_words_host(n * 7 + k * 3 + m, n, k)
+    s = wl.constant_scales_host(n, k, 0x2400)
+    x = wl.small_int_x_host(n + k + 17 * m, m, k)
+    _gemv_case(p, s, x, None, True, "integer-exact random shape")
+
+
 @pytest.mark.parametrize("m", [4, 16])
 def test_gemv_integer_exact_small_batch_3b_lm_head(m):
     """The 3B LM head on the vector kernel (M=4) and on the matrix cores with
