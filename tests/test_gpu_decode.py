@@ -377,3 +377,23 @@ def test_small_batch_both_paths_bit_exact(m, monkeypatch):
             wq.wq_gemv(lin[0], lin[1], lin[2], y1)
             check_exact(y1, ref, f"gemv M={m} {n}x{k} vector={vector}")
     monkeypatch.delenv("WQ_SMALL_BATCH_VECTOR", raising=False)
+
+
+@pytest.mark.parametrize("m", [1, 3, 4, 8, 16])
+def test_decode_random_linear_sets_bit_exact(m):
+    """A seeded set of 12 independent linears of random N and K in one call
+    (the grouped kernels' plans: mixed classes, ragged row runs, balanced
+    wave ranges), integer-exact inputs, every output checked."""
+    rng = np.random.default_rng(7000 + m)
+    shapes = [(int(rng.integers(1, 3000)), 32 * int(rng.integers(1, 449))) for _ in range(12)]
+    announce(f"decode random set M={m} shapes={shapes}")
+    host, lins = [], []
+    for n, k in shapes:
+        p = wl.random_words_host(int(rng.integers(1 << 30)), n, k)
+        s = wl.constant_scales_host(n, k, 0x2400)
+        x = wl.small_int_x_host(int(rng.integers(1 << 30)), m, k)
+        host.append((p, s, x))
+        lins.append((to_dev(p), to_dev(s), to_dev(x), nan_out(m, n)))
+    run(lins, m=m)
+    for (p, s, x), lin, (n, k) in zip(host, lins, shapes):
+        check_exact(lin[3], oracle.gemv(p, s, x, n, k), f"M={m} {n}x{k}")

@@ -224,6 +224,27 @@ def _random_small_batch_shapes(count, seed):
     return out
 
 
+def _random_shapes(count, seed, ms):
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(count):
+        n = int(rng.choice([int(rng.integers(1, 64)), int(rng.integers(64, 1200)), int(rng.integers(1200, 6000))]))
+        k = 32 * int(rng.integers(1, 513))
+        out.append((n, k, int(rng.choice(ms))))
+    return out
+
+
+@pytest.mark.parametrize("n,k,m", _random_shapes(16, 2025, [1]) + _random_shapes(16, 2026, list(range(8, 17))),
+                         ids=lambda v: str(v))
+def test_gemv_integer_exact_random_shapes_m1_and_matrix_cores(n, k, m):
+    """Seeded shapes for the batch-1 kernels (every lanes-per-row and
+    groups-per-lane class, ragged N) and the matrix-core kernel (M 8..16)."""
+    p = wl.random_words_host(n * 5 + k * 7 + m, n, k)
+    s = wl.constant_scales_host(n, k, 0x2400)
+    x = wl.small_int_x_host(n + 3 * k + 19 * m, m, k)
+    _gemv_case(p, s, x, None, True, "integer-exact random shape")
+
+
 @pytest.mark.parametrize("n,k,m", _random_small_batch_shapes(24, 2024), ids=lambda v: str(v))
 def test_gemv_integer_exact_small_batch_random_shapes(n, k, m):
     p = wl.random_words_host(n * 7 + k * 3 + m, n, k)
