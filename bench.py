@@ -598,8 +598,9 @@ def attention_configs(device, seed, only=None, eager=False):
 
 
 def per_config(device, seed):
-    """Per-shape figures beside the headline step (SURVEY configs 1-4 and the
-    8B-class step); none of them is the bench value."""
+    """Per-shape figures beside the headline step (the 512 x 512 parity shape,
+    the 3B- and 8B-class single linears, small batches, the 8B-class step,
+    attention and prefill); none of them is the bench value."""
     import torch
 
     from paper_2412_15803_amd import workloads as wl
