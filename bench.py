@@ -56,6 +56,8 @@ def parse_args():
                     help="time only the prefill GEMM shapes (for profiling its kernel)")
     ap.add_argument("--prefill-config", type=int, default=None,
                     help="with --prefill-only: time only this entry of PREFILL_CONFIGS")
+    ap.add_argument("--step-batches", type=str, default=None,
+                    help="time only the 3B-class step at these comma-separated batch sizes (for counters)")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the per-shape figures (single linears, small batches, 8B-class step)")
     return ap.parse_args()
@@ -676,6 +678,18 @@ def main():
             copy_probe(args.copy_probe_mib, device)
         log("timing the prefill GEMM shapes")
         print(json.dumps({"prefill": prefill_configs(device, args.seed, args.prefill_config)}), flush=True)
+        return
+
+    if args.step_batches:
+        from paper_2412_15803_amd import workloads as wl
+
+        ms = [int(v) for v in args.step_batches.split(",")]
+        log(f"timing the 3B-class step at M = {ms}")
+        gen = torch.Generator(device=device)
+        gen.manual_seed(args.seed + 7)
+        steps3 = [(lin.n, lin.k) for lin in wl.LLAMA3B_LAYER] * 28 + [(wl.LLAMA3B_LM_HEAD.n, wl.LLAMA3B_LM_HEAD.k)]
+        res = time_step_batches(steps3, ms, gen, device, args.steps, args.warmup)
+        print(json.dumps({"3B step batches": res}), flush=True)
         return
 
     if args.attention_only:
