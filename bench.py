@@ -122,6 +122,44 @@ def time_steps(lins, arr, steps, warmup, m=1):
     return start.elapsed_time(end) / steps
 
 
+def time_steps_graph(lins, arr, steps, m=1, per_graph=10):
+    """The same step replayed from a HIP graph of `per_graph` wq_decode_linears
+    calls.  The calls are made once on the capture stream first, so the plan
+    is already on the device and the graph holds only the kernel launches;
+    the replay's outputs are checked against that eager call."""
+    import torch
+
+    from paper_2412_15803_amd import wq
+
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        wq.wq_decode_linears(lins, m=m, _array=arr, stream=s)
+    s.synchronize()
+    eager = [y.clone() for *_, y in lins]
+    for *_, y in lins:
+        y.fill_(float("nan"))
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=s):
+        for _ in range(per_graph):
+            wq.wq_decode_linears(lins, m=m, _array=arr, stream=s)
+    graph.replay()
+    torch.cuda.synchronize()
+    for (*_, y), ref in zip(lins, eager):
+        if not torch.equal(y.view(torch.int16), ref.view(torch.int16)):
+            raise RuntimeError("graph replay of the decode step differs from the eager call")
+    reps = max(1, steps // per_graph)
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(reps):
+        graph.replay()
+    end.record()
+    torch.cuda.synchronize()
+    del graph
+    return start.elapsed_time(end) / (reps * per_graph)
+
+
 def cpu_baseline(seed, budget_s):
     """The oracle GEMV (as it stands) on a bounded prefix of the same step:
     layer 0's four linears and the lm_head first, then further layers until
@@ -720,6 +758,8 @@ def main():
     ms_per_step = time_steps(lins, arr, args.steps, args.warmup)
     gbs = step_bytes / (ms_per_step * 1e-3) / 1e9
 
+    ms_graph = time_steps_graph(lins, arr, args.steps)
+
     ms_chained = None
     if args.chained:
         chained = chained_step(lins)
@@ -767,6 +807,7 @@ def main():
         "us_per_step": round(ms_per_step * 1e3, 2),
         "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
         "tokens_per_s_upper_bound": round(1e3 / ms_per_step, 1),
+        "graph_us_per_step": round(ms_graph * 1e3, 2),
         "chained_us_per_step": round(ms_chained * 1e3, 2) if ms_chained else None,
         "higher_is_better": True,
         "scaling": "weak",
