@@ -119,7 +119,7 @@ __device__ __forceinline__ void compute_from(const StepBuf& b, XSlot<MAXG>& xs, 
 // the same loads and the compiler's wait counts stay exact.
 template <int LPR, int GPL>
 __device__ __forceinline__ void issue_from(StepBuf& b, const Step& s, int lane) {
-    issue_step<LPR, GPL>(b, make_rsrc(s.packed, s.scales, s.scale_bytes), s.row, s.ng, lane);
+    issue_step<LPR, GPL, kCpolNonTemporal>(b, make_rsrc(s.packed, s.scales, s.scale_bytes), s.row, s.ng, lane);
 }
 
 // Register buffers in the pipeline: as many steps as fit a budget of
