@@ -721,6 +721,9 @@ def main():
     if args.step_batches:
         from paper_2412_15803_amd import workloads as wl
 
+        if args.copy_probe_mib:
+            copy_probe(args.copy_probe_mib, device)
+
         ms = [int(v) for v in args.step_batches.split(",")]
         log(f"timing the 3B-class step at M = {ms}")
         gen = torch.Generator(device=device)
