@@ -16,6 +16,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "wq_limits.h"
+
 namespace wq {
 namespace dev {
 
@@ -269,7 +271,7 @@ __device__ __forceinline__ void issue_step(StepBuf& b, const LinearRsrc& r, int6
 }
 
 // Whether a linear's codes can be addressed through 32-bit buffer offsets.
-__host__ __device__ inline bool fits_rsrc(int64_t n, int64_t ng) { return n * ng * 16 <= 0xFFFFFFFFll; }
+using wq::fits_rsrc;
 
 // Dot products, segment reduction and fp16 rounding of one step; the rows
 // below nrows are staged in this wave's LDS slice at ylds[yrel + row], to be

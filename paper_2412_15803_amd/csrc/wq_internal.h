@@ -6,6 +6,7 @@
 #include <stdint.h>
 
 #include "wq.h"
+#include "wq_limits.h"
 
 namespace wq {
 
@@ -30,8 +31,8 @@ constexpr int kMatrixCoreMinM = 8;
 // tiled prefill GEMM.
 constexpr int kMaxSmallBatchM = 64;
 
-// y[M][N] for M > kMaxSmallBatchM: 128 x 128 tiles on the matrix cores.
-bool prefill_fits(int64_t n, int64_t k, int64_t m);
+// y[M][N] for M > kMaxSmallBatchM: 128 x 128 tiles on the matrix cores, for
+// the shapes prefill_fits (wq_limits.h) accepts.
 hipError_t launch_prefill(const uint32_t* packed, const uint16_t* scales, const uint16_t* x, uint16_t* y,
                           int64_t n, int64_t k, int64_t m, hipStream_t stream);
 

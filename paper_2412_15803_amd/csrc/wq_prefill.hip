@@ -36,7 +36,7 @@ using namespace dev;
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float float4v __attribute__((ext_vector_type(4)));
 
-constexpr int kBM = 128;
+constexpr int kBM = 128;  // the tile prefill_fits counts blocks of
 constexpr int kBN = 128;
 constexpr int kBK = 64;
 constexpr int kThreads = 256;
@@ -84,7 +84,7 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(const u32x4* __res
         u32x4 b;
         uint32_t s;
     };
-    constexpr uint32_t kOut = 0xFFFFFFF0u;
+    constexpr uint32_t kOut = kPrefillOutOffset;
     const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<uint16_t*>(x), (short)0, (int)((uint32_t)m * (uint32_t)k * 2u), kRawBufferFlags);
     const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
@@ -189,11 +189,6 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(const u32x4* __res
 }
 
 }  // namespace
-
-bool prefill_fits(int64_t n, int64_t k, int64_t m) {
-    const int64_t blocks = ((m + kBM - 1) / kBM) * ((n + kBN - 1) / kBN);
-    return n <= INT32_MAX && k <= INT32_MAX && m <= INT32_MAX && blocks <= INT32_MAX;
-}
 
 hipError_t launch_prefill(const uint32_t* packed, const uint16_t* scales, const uint16_t* x, uint16_t* y,
                           int64_t n, int64_t k, int64_t m, hipStream_t stream) {

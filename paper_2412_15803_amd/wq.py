@@ -13,7 +13,10 @@ from __future__ import annotations
 import ctypes
 import os
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "lib", "libwq.so")
+# The in-tree build.  WQ_LIBRARY names another build of the same library to
+# load instead (the host-sanitizer test loads one built with AddressSanitizer
+# on its host code).
+LIB_PATH = os.environ.get("WQ_LIBRARY") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "lib", "libwq.so")
 
 WQ_OK = 0
 WQ_ERR_INVALID_ARG = 1

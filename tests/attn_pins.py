@@ -201,6 +201,40 @@ def pin_output_is_a_convex_combination(orc):
             assert np.all(wabs[s, h] <= np.abs(col).max(axis=0) + 1e-12)
 
 
+def pin_score_bound_closed_form(orc):
+    """smax[s, h] = |scale| * max_t sum_d |q_d K_t,d|, worked by hand on a
+    case where it differs from the largest signed score, from the largest
+    |signed score| and from the same bound without |scale|.
+
+    Pages of 2 tokens, sequence 0 of 3 tokens in pages [1, 0] (so token 2
+    is slot 0 of page 0; slot 1 of page 0 holds an unused key of 9s), one
+    empty sequence, 4 query heads on 2 kv heads, scale = -1/2.
+      kv head 0: K_0 = (-1,-1,2,1), K_1 = (-2,1,0,1), K_2 = (0,0,4,0)
+      kv head 1: K_0 = (1,1,1,1),   K_1 = (-3,0,0,0), K_2 = (0,-1,0,0)
+      q_0 = (1,-2,0,3)  on kv 0: sum|qK| = 6, 7, 0 -> 7  (signed 4, -1, 0)
+      q_1 = (0,0,1,0)   on kv 0: sum|qK| = 2, 0, 4 -> 4
+      q_2 = (1,-2,0,3)  on kv 1: sum|qK| = 6, 3, 2 -> 6  (on kv 0 it would be 7)
+      q_3 = (-1,0,0,0)  on kv 1: sum|qK| = 1, 3, 0 -> 3  (signed -1, 3, 0)
+    so smax = (3.5, 2, 3, 1.5) for sequence 0 and 0 for the empty one."""
+    d, page = 4, 2
+    k = np.zeros((2, 2, page, d), dtype=np.float16)
+    keys = {0: [(-1, -1, 2, 1), (-2, 1, 0, 1), (0, 0, 4, 0)],
+            1: [(1, 1, 1, 1), (-3, 0, 0, 0), (0, -1, 0, 0)]}
+    where = [(1, 0), (1, 1), (0, 0)]           # (page, slot) of tokens 0, 1, 2
+    for kvh, rows in keys.items():
+        for (pg, sl), row in zip(where, rows):
+            k[pg, kvh, sl] = row
+    k[0, :, 1] = 9.0                           # the unused slot
+    v = np.ones_like(k)
+    q = np.zeros((2, 4, d), dtype=np.float16)
+    q[0] = [(1, -2, 0, 3), (0, 0, 1, 0), (1, -2, 0, 3), (-1, 0, 0, 0)]
+    q[1] = q[0]
+    table = np.array([[1, 0], [-1, -1]], dtype=np.int32)
+    lens = np.array([3, 0], dtype=np.int32)
+    _, _, smax = orc.decode_attention_f64(q, k, v, table, lens, -0.5)
+    assert np.array_equal(smax, np.array([[3.5, 2.0, 3.0, 1.5], [0.0, 0.0, 0.0, 0.0]])), smax
+
+
 # --------------------------------------------------------------- tolerance
 
 def pin_tolerance_scale(orc):
@@ -245,5 +279,6 @@ ALL_PINS = [
     pin_common_score_shift_is_irrelevant,
     pin_output_is_a_convex_combination,
     pin_tolerance_scale,
+    pin_score_bound_closed_form,
     pin_rejects_invalid_tables,
 ]

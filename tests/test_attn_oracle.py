@@ -38,6 +38,12 @@ MUTANTS = [
      "return ~(diff > attn_tol_bound(wabs))"),
     ("page range not checked", "if np.any(used < 0) or np.any(used >= num_pages):",
      "if np.any(used < 0):"),
+    ("score bound from signed scores", "smax[s, h] = abs(scale) * np.max(np.abs(kk) @ np.abs(qq))",
+     "smax[s, h] = scale * np.max(kk @ qq)"),
+    ("score bound without abs(scale)", "smax[s, h] = abs(scale) * np.max(np.abs(kk) @ np.abs(qq))",
+     "smax[s, h] = scale * np.max(np.abs(kk) @ np.abs(qq))"),
+    ("score bound from |signed scores|", "smax[s, h] = abs(scale) * np.max(np.abs(kk) @ np.abs(qq))",
+     "smax[s, h] = abs(scale) * np.max(np.abs(kk @ qq))"),
 ]
 
 
