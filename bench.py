@@ -106,6 +106,8 @@ def chained_step(lins):
 
 
 def time_steps(lins, arr, steps, warmup, m=1):
+    """Milliseconds per step over `steps` back-to-back wq_decode_linears
+    calls after `warmup` untimed ones, from events on the launch stream."""
     import torch
 
     from paper_2412_15803_amd import wq
@@ -122,11 +124,11 @@ def time_steps(lins, arr, steps, warmup, m=1):
     return start.elapsed_time(end) / steps
 
 
-def time_steps_graph(lins, arr, steps, m=1, per_graph=10):
-    """The same step replayed from a HIP graph of `per_graph` wq_decode_linears
-    calls.  The calls are made once on the capture stream first, so the plan
-    is already on the device and the graph holds only the kernel launches;
-    the replay's outputs are checked against that eager call."""
+def step_graph(lins, arr, m=1, per_graph=10):
+    """A HIP graph of `per_graph` wq_decode_linears calls of the step on a
+    side stream.  The call is made once on that stream first, so its plan is
+    resident and the graph holds only the kernel launches; one replay is
+    checked bit for bit against that eager call.  Returns (graph, calls)."""
     import torch
 
     from paper_2412_15803_amd import wq
@@ -149,15 +151,73 @@ def time_steps_graph(lins, arr, steps, m=1, per_graph=10):
     for (*_, y), ref in zip(lins, eager):
         if not torch.equal(y.view(torch.int16), ref.view(torch.int16)):
             raise RuntimeError("graph replay of the decode step differs from the eager call")
-    reps = max(1, steps // per_graph)
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    start.record()
-    for _ in range(reps):
-        graph.replay()
-    end.record()
-    torch.cuda.synchronize()
+    return graph, per_graph
+
+
+def step_spread(lins, arr, steps, rounds=5):
+    """Five rounds, each one eager run of `steps` back-to-back calls and one
+    run of the same number of calls replayed from a HIP graph, alternated so
+    that neither form gets the cooler start: per-step times (ms) of both."""
+    import torch
+
+    from paper_2412_15803_amd import wq
+
+    graph, per = step_graph(lins, arr)
+    reps = max(1, steps // per)
+    eager, replay = [], []
+    for _ in range(rounds):
+        a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(steps):
+            wq.wq_decode_linears(lins, _array=arr)
+        e.record()
+        torch.cuda.synchronize()
+        eager.append(a.elapsed_time(e) / steps)
+        a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            graph.replay()
+        e.record()
+        torch.cuda.synchronize()
+        replay.append(a.elapsed_time(e) / (reps * per))
     del graph
-    return start.elapsed_time(end) / (reps * per_graph)
+    return eager, replay
+
+
+def _spread(ms_list, nbytes):
+    v = sorted(ms_list)
+    med = v[len(v) // 2]
+    return {"runs": len(v), "us_median": round(med * 1e3, 2), "us_range": [round(v[0] * 1e3, 2), round(v[-1] * 1e3, 2)],
+            "GB_s_median": round(nbytes / (med * 1e-3) / 1e9, 1)}
+
+
+def cpu_model():
+    """The host CPU's model name from /proc/cpuinfo (or the platform's)."""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.lower().startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
+
+
+def blas_threads():
+    """NumPy's BLAS library and its thread count (threadpoolctl, else the
+    usual environment variables)."""
+    try:
+        from threadpoolctl import threadpool_info
+
+        info = [d for d in threadpool_info() if d.get("user_api") == "blas"]
+        if info:
+            return {"library": info[0].get("internal_api"), "threads": info[0].get("num_threads")}
+    except Exception:
+        pass
+    for var in ("OPENBLAS_NUM_THREADS", "OMP_NUM_THREADS", "MKL_NUM_THREADS"):
+        if os.environ.get(var):
+            return {"library": None, "threads": int(os.environ[var]), "from": var}
+    return {"library": None, "threads": None}
 
 
 def cpu_baseline(seed, budget_s):
@@ -194,9 +254,12 @@ def cpu_baseline(seed, budget_s):
         "cores": 1,
         "kind": "oracle",
         "all_cores": threaded,
+        "cpu_model": cpu_model(),
+        "cores_available": len(os.sched_getaffinity(0)),
+        "blas": blas_threads(),
         "sample": f"{len(done)} of 113 linears of the same step ({done[0]} .. {done[-1]}, incl. lm_head), "
-                  f"{done_bytes / 1e9:.3f} GB in {t_total:.1f} s; NumPy elementwise + fp64 sums, one thread "
-                  f"(host {platform.processor() or platform.machine()}, {len(os.sched_getaffinity(0))} cores available)",
+                  f"{done_bytes / 1e9:.3f} GB in {t_total:.1f} s; NumPy elementwise + fp64 sums (the oracle's "
+                  f"GEMV uses no BLAS call), one thread, baseline not target",
     }
 
 
@@ -297,6 +360,108 @@ def time_gemv_rotated(n, k, ms_list, gen, device, calls=200, reps=5):
     del ws
     torch.cuda.empty_cache()
     return out
+
+
+def stream_read_ceiling(device, gib=2, calls=10, reps=5):
+    """GB/s of the library's plain streaming-read probe (wq_stream_read) over
+    a `gib` GiB buffer (8x the 256 MB last-level cache): events around
+    `calls` back-to-back reads, median and range of `reps` such runs."""
+    import torch
+
+    from paper_2412_15803_amd import wq
+
+    buf = torch.ones(gib << 28, dtype=torch.int32, device=device)
+    sink = torch.zeros(2048, dtype=torch.int32, device=device)
+    nbytes = buf.numel() * 4
+    wq.stream_read(buf, sink)
+    torch.cuda.synchronize()
+    rates = []
+    for _ in range(reps):
+        a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(calls):
+            wq.stream_read(buf, sink)
+        e.record()
+        torch.cuda.synchronize()
+        rates.append(nbytes * calls / (a.elapsed_time(e) * 1e-3) / 1e9)
+    del buf, sink
+    torch.cuda.empty_cache()
+    rates.sort()
+    med = rates[len(rates) // 2]
+    return {"kernel": "stream_read_kernel (wq_stream_read)", "bytes": nbytes, "GB_s_median": round(med, 1),
+            "GB_s_range": [round(rates[0], 1), round(rates[-1], 1)], "frac_of_peak": round(med / HBM_PEAK_GBS, 4),
+            "method": f"{calls} back-to-back reads of a {gib} GiB buffer per run, {reps} runs"}
+
+
+def time_layer_calls(shapes, gen, device, calls=200, reps=5):
+    """One decode layer's linears (independent, as BASELINE-style per-layer
+    configs give them) as ONE wq_decode_linears call, cold: the calls rotate
+    over >= 1 GiB of copies of the layer's weights (one descriptor list per
+    copy, each plan made resident by an eager pass first) and are replayed
+    from a HIP graph, so host launch cost is not counted."""
+    import torch
+
+    from paper_2412_15803_amd import workloads as wl
+    from paper_2412_15803_amd import wq
+
+    per = sum(wl.ideal_bytes(n, k, 1) for n, k in shapes)
+    r = max(1, -(-(1 << 30) // per))
+    copies = []
+    for _ in range(r):
+        lins = []
+        for n, k in shapes:
+            p, sc = random_linear(n, k, gen, device)
+            x = torch.randn((1, k), device=device, generator=gen).to(torch.float16)
+            lins.append((p, sc, x, torch.empty((1, n), dtype=torch.float16, device=device)))
+        copies.append((lins, wq.make_linear_array(lins, 1)))
+    s = torch.cuda.Stream(device)
+    s.wait_stream(torch.cuda.current_stream(device))
+    with torch.cuda.stream(s):
+        for lins, arr in copies:
+            wq.wq_decode_linears(lins, m=1, _array=arr, stream=s)
+    s.synchronize()
+    ref = [y.clone() for lins, _ in copies for *_, y in lins]
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=s):
+        for i in range(calls):
+            lins, arr = copies[i % r]
+            wq.wq_decode_linears(lins, m=1, _array=arr, stream=s)
+    times = []
+    for _ in range(reps):
+        a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        graph.replay()
+        e.record()
+        torch.cuda.synchronize()
+        times.append(a.elapsed_time(e) / calls)
+    got = [y for lins, _ in copies for *_, y in lins]
+    if not all(torch.equal(g, t) for g, t in zip(got, ref)):
+        raise RuntimeError("graph replay of the layer calls differs from the eager calls")
+    del graph, copies, ref, got
+    torch.cuda.empty_cache()
+    times.sort()
+    ms = times[len(times) // 2]
+    gbs = per / (ms * 1e-3) / 1e9
+    return {"us": round(ms * 1e3, 2), "us_range": [round(times[0] * 1e3, 2), round(times[-1] * 1e3, 2)],
+            "GB_s": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4), "bytes": per, "copies": r}
+
+
+def layer_configs(device, seed):
+    """The 3B- and 8B-class layers (qkv, o, gate_up, down) at batch 1, each
+    as one wq_decode_linears call per layer."""
+    import torch
+
+    from paper_2412_15803_amd import workloads as wl
+
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed + 11)
+    res = {"method": "one wq_decode_linears call per layer (its four linears in one launch), rotated over >= 1 GiB "
+                     "of layer copies, replayed from a HIP graph; median of 5 runs of 200 calls"}
+    for label, layer in (("3B layer", wl.LLAMA3B_LAYER), ("8B layer", wl.LLAMA8B_LAYER)):
+        shapes = [(lin.n, lin.k) for lin in layer]
+        res[f"{label} " + ", ".join(f"{lin.name} {lin.n}x{lin.k}" for lin in layer)] = time_layer_calls(shapes, gen,
+                                                                                                         device)
+    return res
 
 
 def time_step_batches(shapes, batches, gen, device, steps, warmup):
@@ -669,16 +834,21 @@ def per_config(device, seed):
     return res
 
 
-def profiled_traffic():
-    """HBM bytes per step launch from the committed counter summary, or None
-    when the kernels changed since the counters were taken."""
+def profiled_step():
+    """The committed rocprofv3 summary of the step kernel: HBM bytes per
+    launch and its trace statistics, or None when the kernel's sources have
+    changed since it was taken."""
     from paper_2412_15803_amd.build import source_hash
-    from paper_2412_15803_amd.profsum import parse_traffic
+    from paper_2412_15803_amd.profsum import parse_summary
 
-    got = parse_traffic(STEP_PROFILE)
-    if got is None or got[0] != source_hash():
+    got = parse_summary(STEP_PROFILE)
+    if got is None or got.get("source_hash") != source_hash():
         return None
-    return got[1]
+    out = {"summary": os.path.relpath(STEP_PROFILE, ROOT), "traffic": float(got["traffic_bytes_per_launch"])}
+    for key in ("median_duration_us", "avg_duration_us", "launches_summarised"):
+        if key in got:
+            out[key] = float(got[key])
+    return out
 
 
 def copy_probe(mib, device):
@@ -756,28 +926,41 @@ def main():
         copy_probe(args.copy_probe_mib, device)
 
     log(f"timing {args.steps} steps after {args.warmup} warmup steps")
-    # One persistent-kernel launch per step: the events on the launch stream
-    # around K back-to-back launches give the kernel's average duration.
+    # One grouped launch per step: the events on the launch stream around K
+    # back-to-back launches give the kernel's average duration.
     ms_per_step = time_steps(lins, arr, args.steps, args.warmup)
     gbs = step_bytes / (ms_per_step * 1e-3) / 1e9
+    # Spread: five more runs of K eager calls, alternated with five runs of K
+    # calls replayed from a HIP graph.
+    eager_runs, graph_runs = step_spread(lins, arr, args.steps)
+    spread = {"eager": _spread(eager_runs, step_bytes), "graph": _spread(graph_runs, step_bytes)}
+    ms_graph = sorted(graph_runs)[len(graph_runs) // 2]
 
-    ms_graph = time_steps_graph(lins, arr, args.steps)
 
     ms_chained = None
     if args.chained:
         chained = chained_step(lins)
         ms_chained = time_steps(chained, wq.make_linear_array(chained, 1), args.steps, args.warmup)
 
+    prof = profiled_step()
     roofline = {
         "bound": "hbm",
         "achieved": round(gbs, 1),
         "peak": HBM_PEAK_GBS,
         "unit": "GB/s",
         "frac": round(gbs / HBM_PEAK_GBS, 4),
-        "traffic": profiled_traffic(),
-        "kernel": f"grouped_m1_kernel (one launch per step, avg {ms_per_step * 1e3:.2f} us, "
-                  f"{step_bytes / 1e6:.2f} MB algorithmic per launch)",
+        "traffic": prof["traffic"] if prof else None,
+        "kernel": f"grouped_m1_kernel, one launch per step: {ms_per_step * 1e3:.2f} us per launch, the average over "
+                  f"the {args.steps} timed launches from HIP events on the launch stream; "
+                  f"{step_bytes / 1e6:.2f} MB algorithmic per launch",
+        "profile": prof,
     }
+
+    log("timing the streaming-read probe (achievable-bandwidth context)")
+    ceiling = stream_read_ceiling(device)
+
+    log("timing the 3B- and 8B-class layers as one call per layer")
+    layers = layer_configs(device, args.seed)
 
     dependent = None
     if not args.no_configs:
@@ -810,7 +993,10 @@ def main():
         "us_per_step": round(ms_per_step * 1e3, 2),
         "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
         "tokens_per_s_upper_bound": round(1e3 / ms_per_step, 1),
-        "graph_us_per_step": round(ms_graph * 1e3, 2),
+        "step_runs": spread,
+        "graph_us_per_step": round(ms_graph * 1e3, 2),  # median of the graph runs
+        "stream_read_ceiling": ceiling,
+        "layer_calls": layers,
         "chained_us_per_step": round(ms_chained * 1e3, 2) if ms_chained else None,
         "higher_is_better": True,
         "scaling": "weak",

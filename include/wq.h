@@ -5,7 +5,9 @@
  * The operation is the decode-step linear layer of a 4-bit weight-quantized
  * decoder LLM (WebLLM, Sec. 1 and Sec. 3 / Table 1: token-by-token decoding
  * of 4-bit quantized 1-8B models; Sec. 2.3: weights converted ahead of time,
- * dequantization fused into the matrix-vector kernel):
+ * graph-level kernel fusion and operator-level GEMM tiling).  Dequantizing
+ * the codes in registers inside the matrix-vector kernel is this library's
+ * design, not a detail the paper gives:
  *
  *     y[m][n] = sum_k x[m][k] * w_hat[n][k],   w_hat[n][k] = s16[n][k/32] * (q[n][k] - 8)
  *
@@ -23,8 +25,9 @@
  *
  * Conventions shared by every entry point:
  *   - All data pointers are DEVICE pointers, allocated and owned by the
- *     caller.  The library keeps no reference to them after the call returns
- *     (wq_decode_linears copies the descriptor array, see there).
+ *     caller; they must stay valid until the queued work has run (and, for
+ *     work captured into a graph, for as long as the graph is replayed).
+ *     The buffers the library owns itself are listed at wq_decode_linears.
  *   - `stream` is a hipStream_t passed as void*; NULL is the null stream.
  *     Calls are asynchronous and stream-ordered: they return after queuing
  *     work.  A device fault surfaces at the caller's next synchronization.
@@ -127,11 +130,34 @@ typedef struct wq_linear {
  * running the linears one after another.  No y may overlap the x of the
  * same linear, nor the packed_w or scales of any linear in the list.
  *
- *   linears   HOST array of `count` descriptors; copied during the call, so
- *             it may be freed or reused as soon as the call returns.
+ *   linears   HOST array of `count` descriptors; read during the call
+ *             only, so it may be freed or reused as soon as the call returns.
  *   count     1 <= count <= WQ_MAX_LINEARS.
  *   M, group  shared by all linears (1 <= M <= WQ_MAX_M, group == 32).
- * Errors: as wq_gemv, checked for every descriptor before anything runs.
+ *
+ * Library-owned resources.  For M <= 64 the call turns the list into a
+ * launch plan (about 76 bytes per linear) that the kernels read from device
+ * memory.  Per (device, stream) pair it is called with, the library keeps,
+ * until the process ends: up to 32 device plan buffers holding the plans of
+ * the most recently used distinct descriptor lists, any number of frozen
+ * plan buffers (below), two pinned host staging buffers, and two events.
+ * They are allocated on first use and grown when a longer list needs it.
+ * A list whose plan is already resident is launched without any copy.
+ *
+ * Host blocking.  The call returns after queuing work, except that it waits
+ * (a) for the stream to drain when a plan buffer must grow, and (b) for the
+ * older of two uploads still in flight when a third distinct list arrives
+ * before the device has read either.  Two lists used alternately never wait.
+ *
+ * Stream capture.  When `stream` is capturing, the call records kernel
+ * launches only: if the list's plan is resident (the same call was made on
+ * this stream outside capture before), its buffer is frozen -- never
+ * rewritten or freed -- so the captured graph stays valid for the life of the
+ * process, whatever calls follow.  Otherwise the call returns
+ * WQ_ERR_UNSUPPORTED and captures nothing.
+ *
+ * Errors: as wq_gemv, checked for every descriptor before anything runs;
+ * UNSUPPORTED as above.
  */
 wq_status wq_decode_linears(const wq_linear* linears, int64_t count,
                             int64_t M, int64_t group, void* stream);

@@ -42,7 +42,8 @@ COMPILE_FLAGS = [
 
 
 # Sources the batch-1 decode-step kernel and its launch plan are built from.
-STEP_KERNEL_SOURCES = ("wq_api.hip", "wq_decode.hip", "wq_device.h", "wq_internal.h")
+STEP_KERNEL_SOURCES = ("wq_api.hip", "wq_decode.hip", "wq_device.h", "wq_internal.h", "wq_limits.h", "wq_plan.h",
+                       "wq_plan.hip")
 
 
 def source_hash(names=STEP_KERNEL_SOURCES) -> str:

@@ -14,6 +14,10 @@ namespace wq {
 // wq_last_error_message returns) and returns `st`.
 wq_status record_error(wq_status st, const char* message);
 
+// WQ_OK for hipSuccess; otherwise WQ_ERR_HIP with the runtime's message,
+// recorded as the thread's last error message for entry point `fn`.
+wq_status hip_error(const char* fn, hipError_t e);
+
 // Quantize + pack: one thread per (row, group).
 hipError_t launch_pack(const float* w, uint32_t* packed, uint16_t* scales,
                        int64_t n, int64_t k, hipStream_t stream);

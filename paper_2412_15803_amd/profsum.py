@@ -44,11 +44,17 @@ def _copy_value(entries):
     return max(copies)
 
 
-def _durations(trace_dir, kernel):
+def _durations(trace_dir, kernel, skip=0, take=0):
+    """Durations (us) of the kernel's launches in start order; with skip/take
+    only launches [skip, skip + take) of them (take 0: all after skip)."""
     trace = [r for r in _rows(trace_dir, "*kernel_trace.csv") if kernel in r["Kernel_Name"]]
     if not trace:
         raise SystemExit(f"kernel {kernel!r} not in the trace")
-    return [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in trace]
+    trace.sort(key=lambda r: int(r["Start_Timestamp"]))
+    sel = trace[skip:skip + take] if take else trace[skip:]
+    if not sel:
+        raise SystemExit(f"no launches of {kernel!r} left after skipping {skip}")
+    return [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in sel]
 
 
 def _traffic(fetch, write, f_scale, w_scale, kernel):
@@ -60,7 +66,8 @@ def _traffic(fetch, write, f_scale, w_scale, kernel):
 
 
 def summarise(args):
-    durs = _durations(args.trace, args.kernel)
+    durs = _durations(args.trace, args.kernel, args.skip, args.take)
+    med = statistics.median(durs)
     fetch = _counter(args.fetch, "FETCH_SIZE")
     write = _counter(args.write, "WRITE_SIZE")
     copy_kib = args.copy_mib * 1024.0
@@ -89,9 +96,13 @@ def summarise(args):
         "| Figure | Value |",
         "|---|---|",
         f"| kernel | `{args.kernel}` |",
-        f"| launches in the trace | {len(durs)} |",
-        f"| duration avg / min / max (us) | {avg:.2f} / {min(durs):.2f} / {max(durs):.2f} |",
+        f"| launches summarised | {len(durs)}"
+        + (f" (the kernel's launches {args.skip}..{args.skip + len(durs) - 1} in start order: {args.select})"
+           if args.skip or args.take else "") + " |",
+        f"| duration median / avg / min / max (us) | {med:.2f} / {avg:.2f} / {min(durs):.2f} / {max(durs):.2f} |",
         f"| algorithmic bytes per launch | {args.algo_bytes:,} |",
+        f"| achieved (algorithmic bytes / median duration) | {args.algo_bytes / (med * 1e3):.1f} GB/s"
+        f" = {args.algo_bytes / (med * 1e3) / 8000:.4f} of 8 TB/s |",
         f"| achieved (algorithmic bytes / avg duration) | {args.algo_bytes / (avg * 1e3):.1f} GB/s |",
         f"| FETCH_SIZE per launch (raw KiB, mean of {len(kf)}) | {statistics.mean(kf):,.1f} |",
         f"| WRITE_SIZE per launch (raw KiB, mean of {len(kw)}) | {statistics.mean(kw):,.1f} |",
@@ -110,6 +121,8 @@ def summarise(args):
         f"source_hash: {src_hash}",
         f"traffic_bytes_per_launch: {traffic:.0f}",
         f"avg_duration_us: {avg:.3f}",
+        f"median_duration_us: {med:.3f}",
+        f"launches_summarised: {len(durs)}",
         "```",
         "",
     ]
@@ -118,8 +131,9 @@ def summarise(args):
     print("\n".join(lines))
 
 
-def parse_traffic(path):
-    """(source_hash, traffic bytes per launch) from a summary written above, or None."""
+def parse_summary(path):
+    """The machine-readable block of a summary written above as a dict of
+    strings, or None (no file, or no source hash and traffic in it)."""
     try:
         with open(path) as fh:
             text = fh.read()
@@ -127,10 +141,18 @@ def parse_traffic(path):
         return None
     vals = {}
     for line in text.splitlines():
-        if ":" in line:
+        if ":" in line and not line.startswith("|"):
             k, _, v = line.partition(":")
             vals[k.strip()] = v.strip()
     if "source_hash" not in vals or "traffic_bytes_per_launch" not in vals:
+        return None
+    return vals
+
+
+def parse_traffic(path):
+    """(source_hash, traffic bytes per launch) from a summary written above, or None."""
+    vals = parse_summary(path)
+    if vals is None:
         return None
     return vals["source_hash"], float(vals["traffic_bytes_per_launch"])
 
@@ -149,6 +171,9 @@ def main():
     ap.add_argument("--flops", type=int, default=0, help="flops per launch, for a matrix-core kernel")
     ap.add_argument("--sources", default=None,
                     help="comma-separated csrc/ files whose hash marks the summary (default: the step kernel's)")
+    ap.add_argument("--skip", type=int, default=0, help="leave out the kernel's first N launches (warm-up)")
+    ap.add_argument("--take", type=int, default=0, help="then summarise only the next N launches (0: all)")
+    ap.add_argument("--select", default="", help="what the selected launches are, for the summary")
     ap.add_argument("--out", required=True)
     summarise(ap.parse_args())
 

@@ -1,5 +1,5 @@
-"""Thin ctypes binding of the C ABI in include/wq.h, include/wq_attention.h and
-include/wq_fused.h.
+"""Thin ctypes binding of the C ABI in include/wq.h, include/wq_attention.h,
+include/wq_fused.h and include/wq_probe.h.
 
 Only argument marshalling happens here: torch tensors are turned into device
 pointers and sizes, the current HIP stream is passed through, and non-OK
@@ -28,8 +28,9 @@ GROUP = 32
 
 # Every function declared in the headers under include/.
 EXPORTED = ("wq_status_string", "wq_last_error_message", "wq_version", "wq_pack", "wq_gemv",
-            "wq_decode_linears", "wq_paged_attention_workspace_size", "wq_paged_attention",
-            "wq_fused_linears")
+            "wq_decode_linears", "wq_paged_attention_workspace_size",
+            "wq_paged_attention", "wq_fused_linears", "wq_stream_read")
+
 
 PROLOGUE_NONE = 0
 PROLOGUE_RMSNORM = 1
@@ -100,6 +101,8 @@ def lib() -> ctypes.CDLL:
     L.wq_paged_attention.restype = ctypes.c_int
     L.wq_fused_linears.argtypes = [ctypes.POINTER(WqFusedLinear), i64, vp, i64, vp]
     L.wq_fused_linears.restype = ctypes.c_int
+    L.wq_stream_read.argtypes = [vp, i64, vp, vp]
+    L.wq_stream_read.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -302,3 +305,19 @@ def wq_fused_linears(linears, argmax=None, group: int = GROUP, stream=None, _arr
     device = linears[0]["x"].device
     pa = _dev_tensor(argmax.reshape(-1), "argmax", (torch.int32,), (1,)) if argmax is not None else None
     _check(lib().wq_fused_linears(arr, len(arr), pa, group, _stream(stream, device)))
+
+
+# ------------------------------------------------------- measurement probe
+
+def stream_read(buf, sink, stream=None) -> None:
+    """Read the whole device tensor `buf` once (wq_stream_read); `sink` is a
+    device int32/uint32 tensor of at least 2048 elements."""
+    import torch
+
+    if buf.device.type != "cuda" or not buf.is_contiguous():
+        raise ValueError("buf must be a contiguous device tensor")
+    nbytes = buf.numel() * buf.element_size()
+    if sink.device != buf.device or sink.dtype not in (torch.int32, torch.uint32) or sink.numel() < 2048:
+        raise ValueError("sink must be a device int32 tensor of at least 2048 elements")
+    _check(lib().wq_stream_read(ctypes.c_void_p(buf.data_ptr()), nbytes, ctypes.c_void_p(sink.data_ptr()),
+                                _stream(stream, buf.device)))

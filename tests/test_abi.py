@@ -155,6 +155,15 @@ def test_decode_linears_rejects(L):
     # or, on a GPU host, is never attempted here.
 
 
+def test_stream_read_rejects(L):
+    assert L.wq_stream_read(None, 1 << 20, vp(S), None) == 1
+    assert L.wq_stream_read(vp(P), 1 << 20, None, None) == 1
+    assert L.wq_stream_read(vp(P), 0, vp(S), None) == 1
+    assert L.wq_stream_read(vp(P), 1000, vp(S), None) == 1
+    assert L.wq_stream_read(vp(P + 8), 1 << 20, vp(S), None) == 3
+    assert L.wq_stream_read(vp(P), 1 << 20, vp(S + 2), None) == 3
+
+
 def _no_device_visible():
     """True only where no GPU can be reached: no KFD device node and no
     render node.  The test below hands the library fake device addresses,
@@ -184,6 +193,7 @@ res = {
     "decode_m8": L.wq_decode_linears(_linears(3), 3, 8, 32, None),
     "fused": L.wq_fused_linears(_fused(2), 2, None, 32, None),
     "attention": attention(L),
+    "stream_read": L.wq_stream_read(vp(0x100000), 1 << 20, vp(0x200000), None),
 }
 for name, st in res.items():
     print(name, st, L.wq_last_error_message().decode() if st else "")
@@ -193,7 +203,7 @@ for name, st in res.items():
                          env=env)
     assert out.returncode == 0, out.stderr
     lines = out.stdout.strip().splitlines()
-    assert len(lines) == 7, out.stdout
+    assert len(lines) == 8, out.stdout
     for line in lines:
         name, st = line.split()[:2]
         assert st == "4", line

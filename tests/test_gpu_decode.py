@@ -437,3 +437,97 @@ def test_decode_random_linear_sets_bit_exact(m):
     run(lins, m=m)
     for (p, s, x), lin, (n, k) in zip(host, lins, shapes):
         check_exact(lin[3], oracle.gemv(p, s, x, n, k), f"M={m} {n}x{k}")
+
+
+# ------------------------------------------------------- plans and capture
+
+def _int_set(rng, shapes, m):
+    host, lins = [], []
+    for n, k in shapes:
+        p, s = int_linear(rng, n, k, 1 / 4)
+        x = rng.integers(-1, 2, size=(m, k)).astype(np.float16)
+        host.append((p, s, x))
+        lins.append((to_dev(p), to_dev(s), to_dev(x), nan_out(m, n)))
+    return host, lins
+
+
+def _check_set(host, lins, what):
+    for (p, s, x), lin in zip(host, lins):
+        n, k = p.shape[0], p.shape[1] * 8
+        check_exact(lin[3], oracle.gemv(p, s, x, n, k), f"{what} {n}x{k}")
+
+
+# Reusable plan buffers the library keeps per stream (include/wq.h).
+RESIDENT_PLANS = 32
+
+
+def test_alternating_lists_stay_correct():
+    """Two descriptor lists used alternately on one stream (both plans stay
+    resident), then more lists than the resident plans kept per stream, then
+    the first two again: every call's outputs exact."""
+    rng = np.random.default_rng(801)
+    sets = [_int_set(rng, [(int(rng.integers(1, 700)), 32 * int(rng.integers(1, 130))) for _ in range(3)], 1)
+            for _ in range(2)]
+    sets += [_int_set(rng, [(int(rng.integers(1, 300)), 32 * int(rng.integers(1, 50)))], 1)
+             for _ in range(RESIDENT_PLANS + 4)]
+    announce("decode alternating lists")
+    order = [0, 1, 0, 1, 0] + list(range(2, len(sets))) + [0, 1]
+    for i in order:
+        host, lins = sets[i]
+        for lin in lins:
+            lin[3].fill_(float("nan"))
+        run(lins)
+        _check_set(host, lins, f"list {i}")
+
+
+def test_capture_needs_a_resident_plan():
+    """Capturing a call whose plan is not on the device yet is refused
+    (WQ_ERR_UNSUPPORTED, nothing recorded); after one eager call on the same
+    stream the capture records only launches, and the graph still replays
+    correctly after more than the resident-plan count of other lists has
+    passed through that stream."""
+    import torch
+
+    from paper_2412_15803_amd import wq
+
+    rng = np.random.default_rng(802)
+    host, lins = _int_set(rng, [(5120, 3072), (3072, 3072), (16384, 3072), (3072, 8192)], 1)
+    others = [_int_set(rng, [(int(rng.integers(1, 300)), 32 * int(rng.integers(1, 50)))], 1)
+              for _ in range(RESIDENT_PLANS + 4)]
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    # the stream's workspace exists before capture (its set-up is not a
+    # capture-safe operation), but this list's plan is not in it
+    wq.wq_decode_linears(others[0][1], stream=s)
+    s.synchronize()
+    announce("decode capture of a new list")
+    g0 = torch.cuda.CUDAGraph()
+    status = None
+    with torch.cuda.graph(g0, stream=s):
+        try:
+            wq.wq_decode_linears(lins, stream=s)
+        except wq.WQError as e:
+            status = e.status
+    assert status == wq.WQ_ERR_UNSUPPORTED
+    del g0
+    announce("decode capture of a resident list")
+    wq.wq_decode_linears(lins, stream=s)
+    s.synchronize()
+    _check_set(host, lins, "eager")
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        wq.wq_decode_linears(lins, stream=s)
+    for rep in range(3):
+        for oh, ol in others:
+            with torch.cuda.stream(s):
+                wq.wq_decode_linears(ol, stream=s)
+        s.synchronize()
+        for oh, ol in others:
+            _check_set(oh, ol, f"other list, round {rep}")
+        for lin in lins:
+            lin[3].fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        _check_set(host, lins, f"replay {rep}")
+    del g
