@@ -154,13 +154,45 @@ typedef struct wq_linear {
  * this stream outside capture before), its buffer is frozen -- never
  * rewritten or freed -- so the captured graph stays valid for the life of the
  * process, whatever calls follow.  Otherwise the call returns
- * WQ_ERR_UNSUPPORTED and captures nothing.
+ * WQ_ERR_UNSUPPORTED and captures nothing; wq_decode_linears_noalloc needs
+ * no prior call.
  *
  * Errors: as wq_gemv, checked for every descriptor before anything runs;
  * UNSUPPORTED as above.
  */
 wq_status wq_decode_linears(const wq_linear* linears, int64_t count,
                             int64_t M, int64_t group, void* stream);
+
+/* Limits of wq_decode_linears_noalloc. */
+#define WQ_NOALLOC_MAX_LINEARS ((int64_t)1024)
+#define WQ_NOALLOC_SCRATCH_BYTES ((int64_t)131072)
+
+/*
+ * wq_decode_linears_noalloc -- wq_decode_linears for callers that cannot
+ * allocate: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc.  Same arguments, kernels and results (bit for bit) as
+ * wq_decode_linears; it calls no hipMalloc, hipFree or other allocating
+ * routine and takes no host or device memory of its own beyond fixed static
+ * storage.
+ *
+ * The launch plan lives in a fixed device array of WQ_NOALLOC_SCRATCH_BYTES
+ * per device, held until the process ends (its address is looked up on the
+ * first call made with that device current).  Each call rewrites the array
+ * with its own plan through small kernels, queued on `stream` ahead of the
+ * GEMV launches, whose launch arguments carry the plan bytes: no host memory
+ * is read after the call returns, so a call captured into a graph carries its
+ * plan and replays correctly after any other calls.  All calls on one device
+ * share the array: calls or graph replays that overlap in time on different
+ * streams of one device race and give undefined results.  Calls on one
+ * stream are ordered and safe.  The host waits for nothing.
+ *
+ * Errors: as wq_decode_linears; INVALID_ARG also when count exceeds
+ * WQ_NOALLOC_MAX_LINEARS (the plan of that many linears, at most 128 bytes
+ * per linear, always fits the array); UNSUPPORTED on a device numbered 64 or
+ * above.
+ */
+wq_status wq_decode_linears_noalloc(const wq_linear* linears, int64_t count,
+                                    int64_t M, int64_t group, void* stream);
 
 #ifdef __cplusplus
 }

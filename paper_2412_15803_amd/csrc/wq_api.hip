@@ -192,7 +192,7 @@ wq_status place_plan(const char* fn, DecodeWorkspace* ws, const std::vector<unsi
     if (capturing)
         return fail(WQ_ERR_UNSUPPORTED,
                     "%s: the stream is capturing and this descriptor list's plan is not on the device; make the "
-                    "same call once on this stream outside capture first", fn);
+                    "same call once on this stream outside capture first, or use wq_decode_linears_noalloc", fn);
     int reusable = 0;
     PlanSlot* slot = nullptr;
     for (PlanSlot& s : ws->slots) {

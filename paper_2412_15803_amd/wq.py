@@ -28,9 +28,12 @@ GROUP = 32
 
 # Every function declared in the headers under include/.
 EXPORTED = ("wq_status_string", "wq_last_error_message", "wq_version", "wq_pack", "wq_gemv",
-            "wq_decode_linears", "wq_paged_attention_workspace_size",
+            "wq_decode_linears", "wq_decode_linears_noalloc", "wq_paged_attention_workspace_size",
             "wq_paged_attention", "wq_fused_linears", "wq_stream_read")
 
+# Limits of wq_decode_linears_noalloc (include/wq.h).
+NOALLOC_MAX_LINEARS = 1024
+NOALLOC_SCRATCH_BYTES = 131072
 
 PROLOGUE_NONE = 0
 PROLOGUE_RMSNORM = 1
@@ -94,6 +97,8 @@ def lib() -> ctypes.CDLL:
     L.wq_gemv.restype = ctypes.c_int
     L.wq_decode_linears.argtypes = [ctypes.POINTER(WqLinear), i64, i64, i64, vp]
     L.wq_decode_linears.restype = ctypes.c_int
+    L.wq_decode_linears_noalloc.argtypes = [ctypes.POINTER(WqLinear), i64, i64, i64, vp]
+    L.wq_decode_linears_noalloc.restype = ctypes.c_int
     L.wq_paged_attention_workspace_size.argtypes = [i64, i64, i64, i64, i64, ctypes.POINTER(ctypes.c_size_t)]
     L.wq_paged_attention_workspace_size.restype = ctypes.c_int
     L.wq_paged_attention.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, i64, i64, i64,
@@ -210,6 +215,14 @@ def wq_decode_linears(linears, m: int = 1, group: int = GROUP, stream=None, _arr
     arr = _array if _array is not None else make_linear_array(linears, m, group)
     device = linears[0][2].device
     _check(lib().wq_decode_linears(arr, len(arr), m, group, _stream(stream, device)))
+
+
+def wq_decode_linears_noalloc(linears, m: int = 1, group: int = GROUP, stream=None, _array=None) -> None:
+    """wq_decode_linears through the entry point that allocates nothing (its
+    plan lives in the library's fixed per-device array; see include/wq.h)."""
+    arr = _array if _array is not None else make_linear_array(linears, m, group)
+    device = linears[0][2].device
+    _check(lib().wq_decode_linears_noalloc(arr, len(arr), m, group, _stream(stream, device)))
 
 
 # ------------------------------------------------------- paged attention

@@ -155,6 +155,22 @@ def test_decode_linears_rejects(L):
     # or, on a GPU host, is never attempted here.
 
 
+def test_decode_linears_noalloc_rejects(L):
+    arr = _linears(3)
+    assert L.wq_decode_linears_noalloc(None, 3, 1, 32, None) == 1
+    assert L.wq_decode_linears_noalloc(arr, 0, 1, 32, None) == 1
+    assert L.wq_decode_linears_noalloc(_linears(1025), 1025, 1, 32, None) == 1
+    assert "WQ_NOALLOC_MAX_LINEARS" in L.wq_last_error_message().decode()
+    assert L.wq_decode_linears_noalloc(arr, 3, 1, 64, None) == 2
+    assert L.wq_decode_linears_noalloc(arr, 3, 0, 32, None) == 1
+    bad = _linears(3, {(1, "x"): 0x20000000 + 0x2000000 + 8})
+    assert L.wq_decode_linears_noalloc(bad, 3, 1, 32, None) == 3
+    assert "linear 1" in L.wq_last_error_message().decode()
+    clash = _linears(3, {(2, "y"): 0x10000000 + 64})
+    assert L.wq_decode_linears_noalloc(clash, 3, 1, 32, None) == 1
+    assert "overlaps packed_w or scales" in L.wq_last_error_message().decode()
+
+
 def test_stream_read_rejects(L):
     assert L.wq_stream_read(None, 1 << 20, vp(S), None) == 1
     assert L.wq_stream_read(vp(P), 1 << 20, None, None) == 1
@@ -191,6 +207,8 @@ res = {
     "pack": L.wq_pack(vp(0x500000), vp(0x100000), vp(0x200000), 64, 64, 32, None),
     "decode": L.wq_decode_linears(_linears(3), 3, 1, 32, None),
     "decode_m8": L.wq_decode_linears(_linears(3), 3, 8, 32, None),
+    "decode_noalloc": L.wq_decode_linears_noalloc(_linears(3), 3, 1, 32, None),
+    "decode_noalloc_m4": L.wq_decode_linears_noalloc(_linears(3), 3, 4, 32, None),
     "fused": L.wq_fused_linears(_fused(2), 2, None, 32, None),
     "attention": attention(L),
     "stream_read": L.wq_stream_read(vp(0x100000), 1 << 20, vp(0x200000), None),
@@ -203,7 +221,7 @@ for name, st in res.items():
                          env=env)
     assert out.returncode == 0, out.stderr
     lines = out.stdout.strip().splitlines()
-    assert len(lines) == 8, out.stdout
+    assert len(lines) == 10, out.stdout
     for line in lines:
         name, st = line.split()[:2]
         assert st == "4", line
