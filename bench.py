@@ -52,6 +52,8 @@ def parse_args():
                     help="time only the dependent decode step (for profiling the fused kernels)")
     ap.add_argument("--dependent-ctx", type=int, default=0,
                     help="with --dependent-only: cached tokens per layer for attention (0: linears only)")
+    ap.add_argument("--dependent-eager", action="store_true",
+                    help="with --dependent-only: the persistent chain (WQ_FUSED_PERSISTENT=1) launched from the host")
     ap.add_argument("--prefill-only", action="store_true",
                     help="time only the prefill GEMM shapes (for profiling its kernel)")
     ap.add_argument("--prefill-config", type=int, default=None,
@@ -578,7 +580,7 @@ def time_attention_rotated(hq, hkv, lens, page, seed, device, calls=256, reps=5,
     return round(ms * 1e3, 2), round(per / (ms * 1e-3) / 1e9, 1), per
 
 
-def time_dependent_step(lins, device, seed, ctx=4096, steps=20, reps=3):
+def time_dependent_step(lins, device, seed, ctx=4096, steps=20, reps=3, graph=True, persistent=False):
     """The 3B-class step as one token's dependent chain (batch 1), reusing the
     step's packed weights: per layer RMSNorm -> qkv, attention of the 24
     query heads (q = the first 3072 qkv outputs) over a paged cache of `ctx`
@@ -662,29 +664,42 @@ def time_dependent_step(lins, device, seed, ctx=4096, steps=20, reps=3):
             h.copy_(h0)
             wq.wq_fused_linears(chain, argmax=token, _array=chain_arr)
 
+    old_env = os.environ.get("WQ_FUSED_PERSISTENT")
+    os.environ["WQ_FUSED_PERSISTENT"] = "1" if persistent else "0"
     side = torch.cuda.Stream(device)
     side.wait_stream(torch.cuda.current_stream(device))
     with torch.cuda.stream(side):
         step()
     torch.cuda.current_stream(device).wait_stream(side)
     torch.cuda.synchronize()
+    wq.wq_fused_check()
     ref_logits, ref_token = logits.clone(), int(token.item())
-    graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph):
-        step()
+    g = None
+    if graph:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step()
     times = []
     for _ in range(reps):
         a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record()
         for _ in range(steps):
-            graph.replay()
+            if g is not None:
+                g.replay()
+            else:
+                step()
         e.record()
         torch.cuda.synchronize()
         times.append(a.elapsed_time(e) / steps)
         if int(token.item()) != ref_token or not torch.equal(logits, ref_logits):
-            raise RuntimeError("graph replay of the dependent step differs from the eager step")
+            raise RuntimeError("repeated dependent step differs from the first one")
+    wq.wq_fused_check()
+    if old_env is None:
+        os.environ.pop("WQ_FUSED_PERSISTENT", None)
+    else:
+        os.environ["WQ_FUSED_PERSISTENT"] = old_env
     ms = sorted(times)[len(times) // 2]
-    del graph
+    del g
     torch.cuda.empty_cache()
     gbs = step_bytes / (ms * 1e-3) / 1e9
     return {"us_per_token": round(ms * 1e3, 1), "tokens_per_s": round(1e3 / ms, 1), "GB_s": round(gbs, 1),
@@ -917,7 +932,8 @@ def main():
         if args.copy_probe_mib:
             copy_probe(args.copy_probe_mib, device)
         log(f"timing the dependent decode step ({args.dependent_ctx} cached tokens per layer)")
-        res = time_dependent_step(lins, device, args.seed, ctx=args.dependent_ctx, steps=args.steps, reps=3)
+        res = time_dependent_step(lins, device, args.seed, ctx=args.dependent_ctx, steps=args.steps, reps=3,
+                                  graph=not args.dependent_eager, persistent=args.dependent_eager)
         print(json.dumps({"dependent_decode_step": res}), flush=True)
         return
     arr = wq.make_linear_array(lins, 1)
@@ -966,10 +982,15 @@ def main():
     if not args.no_configs:
         log("timing the dependent decode step (fused linears and paged attention)")
         dependent = {
-            "method": "one token's dependent layer chain (batch 1) with the step's weights, replayed from a HIP graph",
-            "linears only (113 fused linears, one wq_fused_linears call)": time_dependent_step(lins, device, args.seed,
-                                                                                              ctx=0),
-            "with attention over 4096 cached tokens per layer": time_dependent_step(lins, device, args.seed, ctx=4096),
+            "method": "one token's dependent layer chain (batch 1) with the step's weights; per-linear: one "
+                      "launch per linear, replayed from a HIP graph; persistent chain: one cooperative launch of the "
+                      "persistent kernel per wq_fused_linears call, launched from the host",
+            "linears only, per-linear launches (graph replay; 113 fused linears, one wq_fused_linears call)":
+                time_dependent_step(lins, device, args.seed, ctx=0),
+            "linears only, persistent chain (WQ_FUSED_PERSISTENT=1, launched from the host)":
+                time_dependent_step(lins, device, args.seed, ctx=0, graph=False, persistent=True),
+            "with attention over 4096 cached tokens per layer, per-linear launches (graph replay)":
+                time_dependent_step(lins, device, args.seed, ctx=4096),
         }
 
     configs = None

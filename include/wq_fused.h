@@ -84,6 +84,34 @@ typedef struct wq_fused_linear {
 wq_status wq_fused_linears(const wq_fused_linear* linears, int64_t count, int32_t* argmax,
                            int64_t group, void* stream);
 
+/*
+ * wq_fused_check -- synchronize `stream`, then report whether a persistent
+ * chain (below) on the current device has given up since the last check.
+ * Returns WQ_ERR_HIP in that case (and clears the condition), WQ_OK
+ * otherwise, or WQ_ERR_HIP for a runtime error of the synchronization.
+ *
+ * How wq_fused_linears runs a chain.  By default each linear is one launch
+ * (the per-linear path).  With WQ_FUSED_PERSISTENT=1 in the environment
+ * (read at every call), when the current device supports cooperative
+ * launches, the stream is not capturing, and every linear's row length is
+ * one of the shapes compiled for it (rows of up to 256 groups, K <= 8192,
+ * codes below 2 GiB, at most 4096 rows per workgroup), the whole chain is
+ * ONE cooperative launch of a persistent kernel instead: one workgroup per
+ * CU, a grid-wide barrier between consecutive linears (each workgroup
+ * publishes a generation number in a flag of its own and waits for all
+ * flags), and the weights of the next linears streamed while the barrier
+ * completes.  Its results are bit-identical to the per-linear path.  (It is
+ * not the default because on MI355X its barrier costs more than a kernel
+ * boundary: see the library's design notes.)  The persistent kernel keeps, per device, a fixed
+ * array of workgroup flags and an epoch word in library memory (no
+ * allocation), so two chains must not run at the same time on one device.
+ * Every wait in it is bounded (half a second per barrier; the environment
+ * variable WQ_CHAIN_TIMEOUT_TICKS sets it in clock ticks, for tests): when a
+ * wait runs out, every workgroup leaves, that call's outputs are undefined,
+ * and the next wq_fused_check reports it.
+ */
+wq_status wq_fused_check(void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -281,6 +281,17 @@ wq_status wq::record_error(wq_status st, const char* message) { return fail(st, 
 
 wq_status wq::hip_error(const char* fn, hipError_t e) { return hip_status(fn, e); }
 
+wq_status wq::resident_plan(const char* fn, hipStream_t stream, const std::vector<unsigned char>& bytes,
+                            const unsigned char*& d_plan, bool& capturing) {
+    capturing = false;
+    wq_status st = capture_state(fn, stream, capturing);
+    if (st != WQ_OK) return st;
+    std::lock_guard<std::mutex> guard(g_ws_mu);
+    DecodeWorkspace* ws = nullptr;
+    if ((st = get_workspace(fn, stream, ws)) != WQ_OK) return st;
+    return place_plan(fn, ws, bytes, stream, capturing, d_plan);
+}
+
 wq_status wq::check_decode_list(const char* fn, const wq_linear* lin, int64_t count, int64_t m, int64_t group,
                                 wq::plan::Span* weights) {
     for (int64_t i = 0; i < count; ++i) {

@@ -21,6 +21,8 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstdlib>
+#include <mutex>
 #include <cstdarg>
 #include <cstdio>
 #include <vector>
@@ -28,6 +30,7 @@
 #include "wq_device.h"
 #include "wq_fused.h"
 #include "wq_internal.h"
+#include "wq_plan.h"
 
 namespace wq {
 namespace fused {
@@ -412,6 +415,437 @@ __global__ __launch_bounds__(kArgThreads) void argmax_kernel(const uint16_t* y, 
     }
 }
 
+// --------------------------------------------------- persistent dependent chain
+//
+// chain_kernel runs a whole dependent chain (one token's layers) in one
+// cooperative launch: every workgroup stays resident, and the boundary
+// between linear j and j + 1 is a grid-wide barrier instead of a kernel
+// boundary.  What the barrier does not hold up is the weight stream: weights
+// depend on nothing, so each compute wave keeps issuing its next steps --
+// across linear boundaries -- while the barrier and the next prologue run.
+//
+// Workgroup: seven compute waves and one I/O wave (two waves per SIMD).
+//   * Compute waves own contiguous ranges of each linear's steps (the steps of
+//     all compute waves of the grid, in order, cover the linear), stream them
+//     through two or three register buffers in one sequence across linears,
+//     and leave their rows' fp32 sums in the workgroup's LDS.  At a linear
+//     boundary they only synchronise inside the workgroup, never wait for
+//     their own loads, and then stage the next linear's x_eff exactly as
+//     fused_m1_kernel does (the first four waves run the same prologue code
+//     and order, so the chain's results are bit-identical to one
+//     fused_m1_kernel launch per linear).
+//   * The I/O wave writes the workgroup's rows of y (residual added, one
+//     rounding) with agent-scope stores, waits for them to complete,
+//     publishes the linear's generation number in the workgroup's own flag,
+//     and polls every workgroup's flag with agent-scope loads until all have
+//     reached it, then lets its compute waves go on.
+// Everything one workgroup reads of another's outputs (x, residuals, flags)
+// is read with agent-scope loads, coherent across the chip's L2 caches
+// without invalidating them, so no barrier writes back or invalidates a
+// cache.
+//
+// Generation numbers continue across launches (a per-device epoch word read
+// at the start and advanced at the end), so no flag is ever reset and a
+// replayed graph needs no clearing.  Every wait is bounded: a poll that runs
+// past `timeout` clock ticks records the launch in the error words and the
+// workgroup leaves; the others see the error word (or time out) and leave
+// too, so every wave ends.
+constexpr int kChainComputeWaves = 7;
+constexpr int kChainPrologueWaves = kWavesPerBlock;  // the compute waves that stage x_eff (256 threads)
+constexpr int kChainThreads = (kChainComputeWaves + 1) * kWave;
+constexpr int kChainYRows = 4096;     // rows of one linear a workgroup stages
+constexpr int kChainMaxBlocks = 1024;
+constexpr uint32_t kChainOut = 0x80000000u;  // offset of unused load slots: past every chain buffer
+
+// Rows per slot of a step: as many as fill `loads` loads.
+__host__ __device__ constexpr int chain_u(int gpl, int loads) { return gpl >= loads ? 1 : loads / gpl; }
+
+// One linear of a chain as the kernel reads it (uploaded once per chain).
+struct ChainLinear {
+    const void* packed;
+    const uint16_t* scales;
+    const uint16_t* x;
+    uint16_t* y;
+    const uint16_t* norm;
+    const uint16_t* residual;
+    int64_t n;
+    int64_t steps;   // ceil(n / rows per step)
+    int32_t ng, lpr, gpl, u;
+    int32_t prologue;
+    float eps;
+};
+static_assert(sizeof(ChainLinear) == 88, "ChainLinear layout");
+
+// Cache policy of an agent-scope access (sc1): coherent between the chip's
+// L2 caches, as relaxed agent-scope atomics are.
+constexpr int kCpolAgent = 16;
+
+static __device__ __align__(256) uint32_t chain_flags[kChainMaxBlocks];
+static __device__ uint32_t chain_epoch;
+static __device__ uint32_t chain_err_flag;  // nonzero: the launch with base chain_err_base gave up
+static __device__ uint32_t chain_err_base;
+
+__device__ __forceinline__ uint32_t ld_agent(const uint32_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_agent(uint32_t* p, uint32_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// First and one-past-last step of compute wave gw (of `waves`) in a linear of
+// `steps` steps.
+__device__ __forceinline__ int64_t chain_step0(int64_t gw, int64_t steps, int64_t waves) { return gw * steps / waves; }
+
+// Issue side: walks the wave's steps in order across linears and issues each
+// step's loads.  Every step issues LOADS code and LOADS scale loads
+// whatever its shape, unused slots pointed past the buffer's end (they
+// return zeros without a memory access), so every path issues the same loads
+// and the compiler's wait counts stay exact.  Past the last linear the loads
+// go to an empty buffer.
+struct ChainIssue {
+    int lin;          // linear being issued (== count: past the end)
+    int64_t step, end;
+    LinearRsrc r;
+    uint32_t lane_w;  // this lane's byte offset within a step (codes; scales take 1/8)
+    int ng, lpr, gpl, u, rows;  // rows per slot, rows per step
+};
+
+__device__ __forceinline__ void chain_issue_enter(ChainIssue& c, const ChainLinear* plan, int count, int64_t gw,
+                                                  int64_t waves, int lane) {
+    while (c.lin < count) {
+        const ChainLinear& L = plan[c.lin];
+        const int64_t sb = chain_step0(gw, L.steps, waves), se = chain_step0(gw + 1, L.steps, waves);
+        if (sb < se) {
+            c.step = sb;
+            c.end = se;
+            c.ng = L.ng;
+            c.lpr = L.lpr;
+            c.gpl = L.gpl;
+            c.u = L.u;
+            c.rows = L.u * (kWave / L.lpr);
+            c.r = make_rsrc(L.packed, L.scales, (uint32_t)(L.n * L.ng * 2));
+            const int slot = lane / c.lpr, sub = lane & (c.lpr - 1);
+            c.lane_w = (uint32_t)(slot * L.u * L.ng + sub) * 16u;
+            return;
+        }
+        ++c.lin;
+    }
+    c.step = c.end = 0;
+    c.r.w = __builtin_amdgcn_make_buffer_rsrc(const_cast<ChainLinear*>(plan), (short)0, 0, kRawBufferFlags);
+    c.r.s = c.r.w;
+    c.lane_w = 0;
+    c.ng = c.lpr = c.gpl = c.u = 1;
+    c.rows = 1;
+}
+
+// Issue the step the cursor is at into b and move on; returns the step's
+// linear (count past the end) and its step index in `step`.
+template <int LOADS>
+__device__ __forceinline__ int chain_issue(ChainIssue& c, StepBuf& b, int64_t& step, const ChainLinear* plan,
+                                           int count, int64_t gw, int64_t waves, int lane) {
+    const int lin = c.lin;
+    step = c.step;
+    const uint32_t g0 = (uint32_t)(c.step * c.rows * c.ng);
+    const uint32_t lane_s = c.lane_w >> 3;
+    const int nloads = lin < count ? c.gpl * c.u : 0;
+    int u = 0, j = 0;
+#pragma unroll
+    for (int k = 0; k < LOADS; ++k) {
+        const bool used = k < nloads;
+        const uint32_t go = g0 + (uint32_t)(u * c.ng + c.lpr * j);
+        const uint32_t sw = used ? go * 16u : kChainOut, ss = used ? go * 2u : kChainOut;
+        b.w[k] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(c.r.w, c.lane_w, sw, kCpolNonTemporal));
+        b.s[k] = __builtin_amdgcn_raw_buffer_load_b16(c.r.s, lane_s, ss, kCpolNonTemporal);
+        if (++j == c.gpl) {
+            j = 0;
+            ++u;
+        }
+    }
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+    if (lin < count && ++c.step >= c.end) {
+        ++c.lin;
+        chain_issue_enter(c, plan, count, gw, waves, lane);
+    }
+    return lin;
+}
+
+// compute_step_f32 for the chain's step shape (U rows per slot from chain_u).
+template <int LPR, int GPL, int MAXG, int LOADS>
+__device__ __forceinline__ void chain_compute(const StepBuf& b, const half2v (&xr)[MAXG][16], int nrows, float* ylds,
+                                              int yrel, int lane) {
+    constexpr int U = chain_u(GPL, LOADS);
+    const int slot = lane / LPR;
+    const int sub = lane & (LPR - 1);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        float acc = 0.0f;
+#pragma unroll
+        for (int j = 0; j < GPL; ++j) {
+            const float s = h2f(b.s[u * GPL + j]);
+            acc = fmaf(s, dot_group(b.w[u * GPL + j], xr[j]), acc);
+        }
+        const float tot = segment_sum<LPR>(acc);
+        const int rr = slot * U + u;
+        if (sub == LPR - 1 && rr < nrows) ylds[yrel + rr] = tot;
+    }
+}
+
+// x_eff of linear L into LDS by the first 256 compute threads: stage_prologue's
+// loads, reduction order and arithmetic (so x_eff is bit-identical), with
+// PROLOGUE_NONE copying x.  Uses one workgroup barrier, two for RMSNorm; the
+// I/O wave takes the same number.
+template <int CPT>
+__device__ __forceinline__ void chain_prologue(const ChainLinear& L, uint16_t* s_x, float* red) {
+    const int tid = threadIdx.x;
+    const int chunks = L.ng * (kGroup / 8);
+    const bool two = L.prologue != WQ_PROLOGUE_NONE;
+    // x (and the up half) may have been written by other workgroups during
+    // this launch: agent-scope loads, which are coherent across the chip's
+    // caches without invalidating them.  The norm weight is read-only.
+    const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(L.x), (short)0, (int)(chunks * 16 * (L.prologue == WQ_PROLOGUE_SILU_MUL ? 2 : 1)),
+        kRawBufferFlags);
+    const WQ_GLOBAL u32x4* ns = gbl(reinterpret_cast<const u32x4*>(L.norm));
+    u32x4 xa[CPT], xb[CPT];
+#pragma unroll
+    for (int r = 0; r < CPT; ++r) {
+        const int c = tid + r * kBlock;
+        if (c < chunks) {
+            xa[r] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rx, (uint32_t)c * 16u, 0, kCpolAgent));
+            if (L.prologue == WQ_PROLOGUE_RMSNORM) xb[r] = ns[c];
+            else if (two)
+                xb[r] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                      rx, (uint32_t)(chunks + c) * 16u, 0, kCpolAgent));
+        }
+    }
+    float inv = 0.0f;
+    if (L.prologue == WQ_PROLOGUE_RMSNORM) {
+        float ss = 0.0f;
+#pragma unroll
+        for (int r = 0; r < CPT; ++r) {
+            if (tid + r * kBlock >= chunks) continue;
+            const uint32_t w[4] = {xa[r].x, xa[r].y, xa[r].z, xa[r].w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float lo = h2f(w[i] & 0xFFFFu), hi = h2f(w[i] >> 16);
+                ss = fmaf(lo, lo, ss);
+                ss = fmaf(hi, hi, ss);
+            }
+        }
+        const float total = block_sum(ss, red);
+        inv = 1.0f / sqrtf(total / (float)(L.ng * kGroup) + L.eps);
+    }
+#pragma unroll
+    for (int r = 0; r < CPT; ++r) {
+        const int c = tid + r * kBlock;
+        if (c >= chunks) continue;
+        if (!two) {
+            reinterpret_cast<u32x4*>(s_x)[c] = xa[r];
+            continue;
+        }
+        const uint32_t wa[4] = {xa[r].x, xa[r].y, xa[r].z, xa[r].w};
+        const uint32_t wb[4] = {xb[r].x, xb[r].y, xb[r].z, xb[r].w};
+        uint32_t o[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            float v[2];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const float p = h2f(h ? wa[i] >> 16 : wa[i] & 0xFFFFu);
+                const float q = h2f(h ? wb[i] >> 16 : wb[i] & 0xFFFFu);
+                v[h] = L.prologue == WQ_PROLOGUE_RMSNORM ? (p * inv) * q : silu(p) * q;
+            }
+            o[i] = f2h(v[0]) | (f2h(v[1]) << 16);
+        }
+        reinterpret_cast<u32x4*>(s_x)[c] = u32x4{o[0], o[1], o[2], o[3]};
+    }
+    __syncthreads();
+}
+
+// This lane's x groups of a linear from x_eff in LDS (load_x_lane_lds with
+// the shape known at run time, one code path for every shape so that xr is
+// assigned in one place): group j < gpl of the lane's row slot, zero where
+// the group index runs past the row and for j >= gpl.
+template <int MAXG>
+__device__ __forceinline__ void chain_x(const uint16_t* s_x, int ng, int lpr, int gpl, int lane,
+                                        half2v (&xr)[MAXG][16]) {
+    const int sub = lane & (lpr - 1);
+#pragma unroll
+    for (int j = 0; j < MAXG; ++j) {
+        const bool act = j < gpl && sub + lpr * j < ng;
+        const u32x4* src = reinterpret_cast<const u32x4*>(s_x + min(sub + lpr * j, ng - 1) * kGroup);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const u32x4 d = src[c];
+            xr[j][4 * c + 0] = as_h2(act ? (d.x & 0xFFFFu) | (d.z << 16) : 0u);
+            xr[j][4 * c + 1] = as_h2(act ? (d.x >> 16) | (d.z & 0xFFFF0000u) : 0u);
+            xr[j][4 * c + 2] = as_h2(act ? (d.y & 0xFFFFu) | (d.w << 16) : 0u);
+            xr[j][4 * c + 3] = as_h2(act ? (d.y >> 16) | (d.w & 0xFFFF0000u) : 0u);
+        }
+        // One group's raw vectors at a time: hoisting every group's LDS reads
+        // ahead of the pairing would hold them all beside the buffers in flight.
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
+// Step shapes are coded lanes-per-row * 16 + groups-per-lane.  A kernel
+// variant compiles the compute of the shapes in its list only: every extra
+// shape in the dispatch raises the register pressure of all of them.
+constexpr int chain_code(int lpr, int gpl) { return lpr * 16 + gpl; }
+
+template <int MAXG, int LOADS, int... S>
+__device__ __forceinline__ void chain_compute_any(int shape, const StepBuf& b, const half2v (&xr)[MAXG][16], int nrows,
+                                                  float* ylds, int yrel, int lane) {
+    ((shape == S ? (chain_compute<S / 16, S % 16, MAXG, LOADS>(b, xr, nrows, ylds, yrel, lane), 0) : 0), ...);
+}
+
+// A variant: MAXG groups of x per lane (the largest groups-per-lane of its
+// shapes), LOADS code loads per step, NB steps in flight per compute wave,
+// and its shapes S.
+template <int MAXG, int LOADS, int NB, int... S>
+__global__ __launch_bounds__(kChainThreads, 2) void chain_kernel(const ChainLinear* __restrict__ plan, int count,
+                                                                 uint64_t timeout) {
+    __shared__ __align__(16) uint16_t s_x[kMaxK];
+    __shared__ __align__(16) float s_y[kChainYRows];
+    __shared__ float s_red[kWavesPerBlock];
+    __shared__ int s_abort;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int nblocks = gridDim.x;
+    const int64_t waves = (int64_t)nblocks * kChainComputeWaves;
+    const uint32_t base = ld_agent(&chain_epoch);
+
+    if (wave == kChainComputeWaves) {
+        // ------------------------------------------------------------ I/O wave
+        for (int j = 0; j < count; ++j) {
+            const ChainLinear& L = plan[j];
+            if (L.prologue == WQ_PROLOGUE_RMSNORM) __syncthreads();
+            __syncthreads();          // x_eff of j staged
+            __syncthreads();          // the compute waves' rows of j are in LDS
+            // This workgroup's rows of j: those of its four compute waves.
+            const int64_t rows = L.u * (kWave / L.lpr);
+            const int64_t gw0 = (int64_t)blockIdx.x * kChainComputeWaves;
+            const int64_t r0 = chain_step0(gw0, L.steps, waves) * rows;
+            const int64_t r1 = min(L.n, chain_step0(gw0 + kChainComputeWaves, L.steps, waves) * rows);
+            for (int64_t r = r0 + lane; r < r1; r += kWave) {
+                float v = s_y[r - r0];
+                if (L.residual)
+                    v += h2f(__hip_atomic_load(L.residual + r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+                __hip_atomic_store(L.y + r, (uint16_t)f2h(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+            // Every value another workgroup reads from this launch's outputs
+            // (x, residuals) is written and read with agent-scope accesses,
+            // so publishing needs no cache write-back: the flag goes out once
+            // the stores above have completed.
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            const uint32_t gen = base + (uint32_t)j + 1u;
+            if (lane == 0) st_agent(&chain_flags[blockIdx.x], gen);
+            // Wait for every workgroup's flag to reach gen.
+            const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+            int abort = 0;
+            for (;;) {
+                bool mine = true;
+                for (int b = lane; b < nblocks; b += kWave) mine &= (int32_t)(ld_agent(&chain_flags[b]) - gen) >= 0;
+                if (__all(mine)) break;
+                if (ld_agent(&chain_err_flag) && ld_agent(&chain_err_base) == base) {
+                    abort = 1;
+                    break;
+                }
+                if (__builtin_amdgcn_s_memrealtime() - t0 > timeout) {
+                    if (lane == 0) {
+                        st_agent(&chain_err_base, base);
+                        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+                        st_agent(&chain_err_flag, 1u);
+                    }
+                    abort = 1;
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(1);
+            }
+            // No cache invalidation either: the reads that depend on the flags
+            // are agent-scope loads issued after the flags were seen.
+            asm volatile("" ::: "memory");
+            if (abort && lane == 0) st_agent(&chain_epoch, base + (uint32_t)count);
+            if (lane == 0) s_abort = abort;
+            __syncthreads();          // released: y of j is visible everywhere
+            if (abort) return;
+        }
+        if (blockIdx.x == 0 && lane == 0) st_agent(&chain_epoch, base + (uint32_t)count);
+        return;
+    }
+
+    // ------------------------------------------------------------ compute waves
+    static_assert(NB == 2 || NB == 3, "chain pipeline depth");
+    static_assert(LOADS <= 8, "a step buffer holds eight loads");
+    const int64_t gw = (int64_t)blockIdx.x * kChainComputeWaves + wave;
+    ChainIssue ic;
+    ic.lin = 0;
+    chain_issue_enter(ic, plan, count, gw, waves, lane);
+    // The register buffers, as separate variables so that nothing is
+    // indexed at run time: each holds one step (its linear and step index).
+    StepBuf b0, b1, b2;
+    int l0, l1, l2 = count;
+    int64_t s0, s1, s2 = 0;
+    l0 = chain_issue<LOADS>(ic, b0, s0, plan, count, gw, waves, lane);
+    l1 = chain_issue<LOADS>(ic, b1, s1, plan, count, gw, waves, lane);
+    if constexpr (NB == 3) l2 = chain_issue<LOADS>(ic, b2, s2, plan, count, gw, waves, lane);
+
+    half2v xr[MAXG][16];
+    int cur = -1;            // linear whose x_eff is in xr
+    int64_t r0 = 0;          // first row this workgroup stages for `cur`
+    int shape = 0;           // lpr * 16 + gpl of `cur`
+    int ng = 1;
+    int64_t n = 0, rows = 1;
+    // Leave linear `cur` (its rows are in LDS) and stage the next one; false
+    // when the I/O wave gave up.
+    auto advance = [&]() __attribute__((always_inline)) -> bool {
+        if (cur >= 0) {
+            __syncthreads();          // rows of cur are in LDS
+            __syncthreads();          // the I/O wave has written them and passed the barrier
+            if (s_abort) return false;
+        }
+        ++cur;
+        if (cur >= count) return true;
+        const ChainLinear& L = plan[cur];
+        if (wave < kChainPrologueWaves) {
+            chain_prologue<MAXG>(L, s_x, s_red);
+        } else {
+            if (L.prologue == WQ_PROLOGUE_RMSNORM) __syncthreads();
+            __syncthreads();
+        }
+        ng = L.ng;
+        n = L.n;
+        rows = L.u * (kWave / L.lpr);
+        shape = L.lpr * 16 + L.gpl;
+        r0 = chain_step0((int64_t)blockIdx.x * kChainComputeWaves, L.steps, waves) * rows;
+        chain_x<MAXG>(s_x, ng, L.lpr, L.gpl, lane, xr);
+        return true;
+    };
+    // Compute the step a buffer holds and refill it with the wave's next
+    // step: 0 to go on, 1 when the wave's steps are done, 2 to leave.
+    auto slot = [&](StepBuf& b, int& lin, int64_t& step) __attribute__((always_inline)) -> int {
+        if (lin >= count) return 1;
+        while (cur < lin)
+            if (!advance()) return 2;
+        const int64_t row = step * rows;
+        const int nrows = (int)min(rows, n - row);
+        chain_compute_any<MAXG, LOADS, S...>(shape, b, xr, nrows, s_y, (int)(row - r0), lane);
+        lin = chain_issue<LOADS>(ic, b, step, plan, count, gw, waves, lane);
+        return 0;
+    };
+    int r = 0;
+    for (;;) {
+        if ((r = slot(b0, l0, s0)) != 0) break;
+        if ((r = slot(b1, l1, s1)) != 0) break;
+        if constexpr (NB == 3)
+            if ((r = slot(b2, l2, s2)) != 0) break;
+    }
+    if (r == 2) return;
+    while (cur < count)
+        if (!advance()) return;
+}
+
 // ------------------------------------------------------------------- host
 
 template <int LPR, int GPL>
@@ -526,6 +960,165 @@ wq_status check_linear(const char* fn, int64_t i, const wq_fused_linear& l) {
     return WQ_OK;
 }
 
+// The compiled chain variants: the two step shapes of the Llama-class 3B
+// layers (K = 3072 and 8192) on their own, then every narrow shape (rows of
+// up to 256 groups).  A chain runs the first variant that has all of its
+// shapes; other chains (rows of more than 256 groups, whose x alone would
+// take 112 or more registers beside the buffers) take the per-linear path.
+struct ChainVariant {
+    const void* fn;
+    int loads;
+    int nshapes;
+    int shapes[8];
+};
+#define WQ_C(L, G) chain_code(L, G)
+#define WQ_NARROW WQ_C(64, 1), WQ_C(64, 2), WQ_C(64, 3), WQ_C(64, 4), WQ_C(32, 1), WQ_C(32, 3), WQ_C(16, 1), WQ_C(16, 3)
+const ChainVariant kChainVariants[] = {
+    {reinterpret_cast<const void*>(chain_kernel<4, 6, 3, WQ_C(32, 3), WQ_C(64, 4)>), 6, 2, {WQ_C(32, 3), WQ_C(64, 4)}},
+    {reinterpret_cast<const void*>(chain_kernel<4, 6, 3, WQ_NARROW>), 6, 8, {WQ_NARROW}},
+};
+#undef WQ_NARROW
+#undef WQ_C
+constexpr int kChainVariantCount = sizeof(kChainVariants) / sizeof(kChainVariants[0]);
+
+// Persistent-chain support of one device: whether cooperative launches work,
+// how many workgroups of each variant are co-resident, the clock rate.
+struct ChainDevice {
+    bool ready = false;
+    bool coop = false;
+    int blocks[kChainVariantCount] = {};
+    uint64_t ticks_per_s = 0;
+};
+constexpr int kChainMaxDevices = 64;
+std::mutex g_chain_mu;
+ChainDevice g_chain_dev[kChainMaxDevices];
+
+hipError_t chain_device(int device, ChainDevice*& out) {
+    out = nullptr;
+    if (device < 0 || device >= kChainMaxDevices) return hipSuccess;
+    ChainDevice& d = g_chain_dev[device];
+    if (!d.ready) {
+        int coop = 0, cus = 0, rate_khz = 0;
+        hipError_t e;
+        if ((e = hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, device)) != hipSuccess) return e;
+        if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device)) != hipSuccess) return e;
+        if ((e = hipDeviceGetAttribute(&rate_khz, hipDeviceAttributeWallClockRate, device)) != hipSuccess) return e;
+        for (int v = 0; v < kChainVariantCount; ++v) {
+            int per = 0;
+            if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kChainVariants[v].fn, kChainThreads, 0)) !=
+                hipSuccess)
+                return e;
+            // One workgroup per CU: its five waves hold two SIMDs' worth of
+            // registers on one of them already.
+            d.blocks[v] = per >= 1 ? std::min(cus, kChainMaxBlocks) : 0;
+        }
+        d.coop = coop != 0;
+        d.ticks_per_s = (uint64_t)(rate_khz > 0 ? rate_khz : 100000) * 1000u;
+        d.ready = true;
+    }
+    out = &d;
+    return hipSuccess;
+}
+
+bool env_flag_off(const char* name) {
+    const char* e = std::getenv(name);
+    return e && e[0] == '0';
+}
+
+bool env_flag_on(const char* name) {
+    const char* e = std::getenv(name);
+    return e && e[0] == '1';
+}
+
+// Run the chain as one persistent cooperative launch when every linear fits
+// its limits; `launched` is false (and nothing queued) when the chain must
+// take the per-linear path instead.
+wq_status launch_chain(const char* fn, const std::vector<wq_fused_linear>& lin, hipStream_t stream, bool& launched) {
+    launched = false;
+    if (!env_flag_on("WQ_FUSED_PERSISTENT")) return WQ_OK;
+    int device = 0;
+    hipError_t e = hipGetDevice(&device);
+    if (e != hipSuccess) return err(WQ_ERR_HIP, "%s: HIP error %d (%s)", fn, (int)e, hipGetErrorString(e));
+    ChainDevice* cd = nullptr;
+    {
+        std::lock_guard<std::mutex> guard(g_chain_mu);
+        if ((e = chain_device(device, cd)) != hipSuccess)
+            return err(WQ_ERR_HIP, "%s: HIP error %d (%s)", fn, (int)e, hipGetErrorString(e));
+    }
+    if (!cd || !cd->coop) return WQ_OK;
+    int variant = -1;
+    for (int v = 0; v < kChainVariantCount && variant < 0; ++v) {
+        bool all = true;
+        for (const wq_fused_linear& l : lin) {
+            int lpr = 64, gpl = 1;
+            pick_shape((int)(l.K / kGroup), lpr, gpl);
+            const int code = chain_code(lpr, gpl);
+            bool found = false;
+            for (int k = 0; k < kChainVariants[v].nshapes; ++k) found = found || kChainVariants[v].shapes[k] == code;
+            all = all && found;
+        }
+        if (all) variant = v;
+    }
+    if (variant < 0) return WQ_OK;
+    const int loads = kChainVariants[variant].loads;
+    const int blocks = cd->blocks[variant];
+    if (blocks < 1) return WQ_OK;
+    const int64_t waves = (int64_t)blocks * kChainComputeWaves;
+    std::vector<unsigned char> bytes(sizeof(ChainLinear) * lin.size());
+    ChainLinear* cl = reinterpret_cast<ChainLinear*>(bytes.data());
+    for (size_t i = 0; i < lin.size(); ++i) {
+        const wq_fused_linear& l = lin[i];
+        ChainLinear& c = cl[i];
+        int lpr = 64, gpl = 1;
+        const int64_t ng = l.K / kGroup;
+        pick_shape((int)ng, lpr, gpl);
+        if (l.N * ng * 16 >= ((int64_t)1 << 31)) return WQ_OK;  // codes past the unused-slot offset
+        const int u = chain_u(gpl, loads);
+        const int64_t rows = (int64_t)u * (kWave / lpr);
+        const int64_t steps = (l.N + rows - 1) / rows;
+        // Rows a workgroup stages: at most four compute waves' ranges.
+        if (kChainComputeWaves * ((steps + waves - 1) / waves) * rows > kChainYRows) return WQ_OK;
+        c.packed = l.packed_w;
+        c.scales = l.scales;
+        c.x = l.x;
+        c.y = l.y;
+        c.norm = l.norm_weight;
+        c.residual = l.residual;
+        c.n = l.N;
+        c.steps = steps;
+        c.ng = (int32_t)ng;
+        c.lpr = lpr;
+        c.gpl = gpl;
+        c.u = u;
+        c.prologue = l.prologue;
+        c.eps = l.eps;
+    }
+    const unsigned char* d_plan = nullptr;
+    bool capturing = false;
+    const wq_status st = resident_plan(fn, stream, bytes, d_plan, capturing);
+    // Under stream capture the chain takes the per-linear path: its launches
+    // are plain kernel nodes.
+    if (capturing) return WQ_OK;
+    if (st != WQ_OK) return st;
+    uint64_t timeout = cd->ticks_per_s / 2;  // half a second per wait
+    if (const char* env = std::getenv("WQ_CHAIN_TIMEOUT_TICKS")) {
+        const long long t = std::atoll(env);
+        if (t > 0) timeout = (uint64_t)t;
+    }
+    const ChainLinear* plan = reinterpret_cast<const ChainLinear*>(d_plan);
+    int count = (int)lin.size();
+    void* args[] = {&plan, &count, &timeout};
+    // WQ_CHAIN_COOPERATIVE=0 (for measurements) launches without the
+    // co-residency guarantee; the bounded waits still end every wave.
+    if (env_flag_off("WQ_CHAIN_COOPERATIVE"))
+        e = hipLaunchKernel(kChainVariants[variant].fn, dim3(blocks), dim3(kChainThreads), args, 0, stream);
+    else
+        e = hipLaunchCooperativeKernel(kChainVariants[variant].fn, dim3(blocks), dim3(kChainThreads), args, 0, stream);
+    if (e != hipSuccess) return err(WQ_ERR_HIP, "%s: HIP error %d (%s)", fn, (int)e, hipGetErrorString(e));
+    launched = true;
+    return WQ_OK;
+}
+
 }  // namespace
 }  // namespace fused
 }  // namespace wq
@@ -573,7 +1166,10 @@ extern "C" wq_status wq_fused_linears(const wq_fused_linear* linears, int64_t co
     }
     (void)hipGetLastError();
     const hipStream_t s = static_cast<hipStream_t>(stream);
-    for (int64_t i = 0; i < count; ++i) {
+    bool launched = false;
+    const wq_status cs = launch_chain(fn, lin, s, launched);
+    if (cs != WQ_OK) return cs;
+    for (int64_t i = 0; !launched && i < count; ++i) {
         const hipError_t e = launch_one(lin[i], s);
         if (e != hipSuccess)
             return err(WQ_ERR_HIP, "%s: linear %lld: HIP error %d (%s)", fn, (long long)i, (int)e, hipGetErrorString(e));
@@ -585,4 +1181,19 @@ extern "C" wq_status wq_fused_linears(const wq_fused_linear* linears, int64_t co
         if (e != hipSuccess) return err(WQ_ERR_HIP, "%s: argmax: HIP error %d (%s)", fn, (int)e, hipGetErrorString(e));
     }
     return WQ_OK;
+}
+
+extern "C" wq_status wq_fused_check(void* stream) {
+    static const char* fn = "wq_fused_check";
+    hipError_t e = hipStreamSynchronize(static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return err(WQ_ERR_HIP, "%s: HIP error %d (%s)", fn, (int)e, hipGetErrorString(e));
+    uint32_t flag = 0;
+    if ((e = hipMemcpyFromSymbol(&flag, HIP_SYMBOL(chain_err_flag), sizeof(flag), 0, hipMemcpyDeviceToHost)) != hipSuccess)
+        return err(WQ_ERR_HIP, "%s: HIP error %d (%s)", fn, (int)e, hipGetErrorString(e));
+    if (!flag) return WQ_OK;
+    const uint32_t zero = 0;
+    if ((e = hipMemcpyToSymbol(HIP_SYMBOL(chain_err_flag), &zero, sizeof(zero), 0, hipMemcpyHostToDevice)) != hipSuccess)
+        return err(WQ_ERR_HIP, "%s: HIP error %d (%s)", fn, (int)e, hipGetErrorString(e));
+    return err(WQ_ERR_HIP, "%s: a persistent chain on this device gave up: a wait between its workgroups ran past "
+               "its time limit, and that call's outputs are undefined", fn);
 }

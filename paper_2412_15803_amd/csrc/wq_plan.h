@@ -11,6 +11,7 @@
 
 #include <algorithm>
 #include <map>
+#include <vector>
 
 #include "wq.h"
 #include "wq_internal.h"
@@ -183,6 +184,15 @@ hipError_t launch_groups(const wq_linear* lin, const Group* groups, int ngroups,
                          hipStream_t stream);
 
 }  // namespace plan
+
+// Place `bytes` in one of the library-owned plan buffers of the current
+// device and `stream` (the resident plans wq_decode_linears keeps, see
+// include/wq.h) and return its device address: no copy when the same bytes
+// are resident already.  Under stream capture only a resident plan is
+// accepted, and its buffer is frozen; otherwise WQ_ERR_UNSUPPORTED is
+// returned and nothing is recorded.  `capturing` reports the stream's state.
+wq_status resident_plan(const char* fn, hipStream_t stream, const std::vector<unsigned char>& bytes,
+                        const unsigned char*& d_plan, bool& capturing);
 
 // Validation shared by the decode-step entry points (defined with the C ABI):
 // every descriptor as for wq_gemv, and no y overlapping any linear's codes or

@@ -32,9 +32,11 @@ def _rows(directory, pattern):
 
 
 def _counter(directory, name):
-    """[(kernel name, grid size, value)] for one counter, one entry per dispatch."""
-    return [(r["Kernel_Name"], int(r["Grid_Size"]), float(r["Counter_Value"]))
-            for r in _rows(directory, "*counter_collection.csv") if r["Counter_Name"] == name]
+    """[(kernel name, grid size, value)] for one counter, one entry per
+    dispatch, in dispatch order."""
+    rows = [r for r in _rows(directory, "*counter_collection.csv") if r["Counter_Name"] == name]
+    rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+    return [(r["Kernel_Name"], int(r["Grid_Size"]), float(r["Counter_Value"])) for r in rows]
 
 
 def _copy_value(entries):
@@ -57,9 +59,13 @@ def _durations(trace_dir, kernel, skip=0, take=0):
     return [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in sel]
 
 
-def _traffic(fetch, write, f_scale, w_scale, kernel):
+def _traffic(fetch, write, f_scale, w_scale, kernel, skip=0, take=0):
+    """Mean scaled fetch and write bytes per dispatch of the kernel; with
+    skip/take only its dispatches [skip, skip + take) in dispatch order."""
     kf = [v for name, _, v in fetch if kernel in name]
     kw = [v for name, _, v in write if kernel in name]
+    kf = kf[skip:skip + take] if take else kf[skip:]
+    kw = kw[skip:skip + take] if take else kw[skip:]
     if not kf or not kw:
         raise SystemExit(f"kernel {kernel!r} not in the counter runs")
     return kf, kw, statistics.mean(kf) * f_scale * 1024.0, statistics.mean(kw) * w_scale * 1024.0
@@ -73,7 +79,8 @@ def summarise(args):
     copy_kib = args.copy_mib * 1024.0
     f_scale = copy_kib / _copy_value(fetch)
     w_scale = copy_kib / _copy_value(write)
-    kf, kw, fetch_b, write_b = _traffic(fetch, write, f_scale, w_scale, args.kernel)
+    kf, kw, fetch_b, write_b = _traffic(fetch, write, f_scale, w_scale, args.kernel, args.counter_skip,
+                                        args.counter_take)
     traffic = fetch_b + write_b
     avg = statistics.mean(durs)
     others = []
@@ -104,7 +111,9 @@ def summarise(args):
         f"| achieved (algorithmic bytes / median duration) | {args.algo_bytes / (med * 1e3):.1f} GB/s"
         f" = {args.algo_bytes / (med * 1e3) / 8000:.4f} of 8 TB/s |",
         f"| achieved (algorithmic bytes / avg duration) | {args.algo_bytes / (avg * 1e3):.1f} GB/s |",
-        f"| FETCH_SIZE per launch (raw KiB, mean of {len(kf)}) | {statistics.mean(kf):,.1f} |",
+        f"| FETCH_SIZE per launch (raw KiB, mean of {len(kf)}"
+        + (f": the kernel's dispatches {args.counter_skip}..{args.counter_skip + len(kf) - 1} of each counter run"
+           if args.counter_skip or args.counter_take else "") + f") | {statistics.mean(kf):,.1f} |",
         f"| WRITE_SIZE per launch (raw KiB, mean of {len(kw)}) | {statistics.mean(kw):,.1f} |",
         f"| copy calibration: FETCH_SIZE / WRITE_SIZE of a {args.copy_mib} MiB copy (raw KiB) | "
         f"{_copy_value(fetch):,.1f} / {_copy_value(write):,.1f} |",
@@ -174,6 +183,8 @@ def main():
     ap.add_argument("--skip", type=int, default=0, help="leave out the kernel's first N launches (warm-up)")
     ap.add_argument("--take", type=int, default=0, help="then summarise only the next N launches (0: all)")
     ap.add_argument("--select", default="", help="what the selected launches are, for the summary")
+    ap.add_argument("--counter-skip", type=int, default=0, help="leave out the kernel's first N dispatches of the counter runs")
+    ap.add_argument("--counter-take", type=int, default=0, help="then use only the next N dispatches (0: all)")
     ap.add_argument("--out", required=True)
     summarise(ap.parse_args())
 

@@ -29,7 +29,7 @@ GROUP = 32
 # Every function declared in the headers under include/.
 EXPORTED = ("wq_status_string", "wq_last_error_message", "wq_version", "wq_pack", "wq_gemv",
             "wq_decode_linears", "wq_decode_linears_noalloc", "wq_paged_attention_workspace_size",
-            "wq_paged_attention", "wq_fused_linears", "wq_stream_read")
+            "wq_paged_attention", "wq_fused_linears", "wq_fused_check", "wq_stream_read")
 
 # Limits of wq_decode_linears_noalloc (include/wq.h).
 NOALLOC_MAX_LINEARS = 1024
@@ -106,6 +106,8 @@ def lib() -> ctypes.CDLL:
     L.wq_paged_attention.restype = ctypes.c_int
     L.wq_fused_linears.argtypes = [ctypes.POINTER(WqFusedLinear), i64, vp, i64, vp]
     L.wq_fused_linears.restype = ctypes.c_int
+    L.wq_fused_check.argtypes = [vp]
+    L.wq_fused_check.restype = ctypes.c_int
     L.wq_stream_read.argtypes = [vp, i64, vp, vp]
     L.wq_stream_read.restype = ctypes.c_int
     _lib = L
@@ -318,6 +320,15 @@ def wq_fused_linears(linears, argmax=None, group: int = GROUP, stream=None, _arr
     device = linears[0]["x"].device
     pa = _dev_tensor(argmax.reshape(-1), "argmax", (torch.int32,), (1,)) if argmax is not None else None
     _check(lib().wq_fused_linears(arr, len(arr), pa, group, _stream(stream, device)))
+
+
+def wq_fused_check(device=None, stream=None) -> None:
+    """Synchronize the stream and raise WQError if a persistent chain on the
+    device gave up since the last check (a bounded wait ran out)."""
+    import torch
+
+    device = torch.device("cuda", torch.cuda.current_device()) if device is None else device
+    _check(lib().wq_fused_check(_stream(stream, device)))
 
 
 # ------------------------------------------------------- measurement probe

@@ -212,6 +212,7 @@ res = {
     "fused": L.wq_fused_linears(_fused(2), 2, None, 32, None),
     "attention": attention(L),
     "stream_read": L.wq_stream_read(vp(0x100000), 1 << 20, vp(0x200000), None),
+    "fused_check": L.wq_fused_check(None),
 }
 for name, st in res.items():
     print(name, st, L.wq_last_error_message().decode() if st else "")
@@ -221,7 +222,7 @@ for name, st in res.items():
                          env=env)
     assert out.returncode == 0, out.stderr
     lines = out.stdout.strip().splitlines()
-    assert len(lines) == 10, out.stdout
+    assert len(lines) == 11, out.stdout
     for line in lines:
         name, st = line.split()[:2]
         assert st == "4", line

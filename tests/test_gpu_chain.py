@@ -1,0 +1,173 @@
+"""The persistent dependent-chain path of wq_fused_linears (one cooperative
+launch per chain, grid-wide barriers between linears; WQ_FUSED_PERSISTENT=1)
+on the GPU, through
+the C ABI: bit for bit the same outputs as the per-linear path (one launch
+per linear, the default), over 3B-class layers with attention's
+place taken by the qkv slice, long random chains of every compiled shape,
+repeated and interleaved calls, and the error path of its bounded waits
+(forced from the host with a one-tick time limit: every wave still ends)."""
+
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+from gpu_util import announce, require_gpu
+from oracle import fused_oracle as fo
+from test_gpu_fused import _h, oracle_linear, random_linear, run_chain
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    require_gpu()
+
+
+def _both_paths(descs, monkeypatch, argmax=False):
+    from paper_2412_15803_amd import wq
+
+    monkeypatch.setenv("WQ_FUSED_PERSISTENT", "1")
+    persistent = run_chain(descs, argmax)
+    wq.wq_fused_check()
+    monkeypatch.setenv("WQ_FUSED_PERSISTENT", "0")
+    per_linear = run_chain(descs, argmax)
+    monkeypatch.delenv("WQ_FUSED_PERSISTENT", raising=False)
+    return persistent, per_linear
+
+
+def _same(a, b, what):
+    bad = np.flatnonzero(a.view(np.uint16) != b.view(np.uint16))
+    assert bad.size == 0, f"{what}: {bad.size} outputs differ, first {bad[:5].tolist()}"
+
+
+def _layers_3b(seed, layers, vocab):
+    """`layers` 3B-class layers (qkv, o + residual, gate_up, down + residual,
+    RMSNorm prologues, the o projection reading the first 3072 qkv outputs)
+    and a final RMSNorm projection of `vocab` rows."""
+    rng = np.random.default_rng(seed)
+    hid, inter = 3072, 8192
+    h = _h(rng.standard_normal(hid))
+    descs = []
+    for l in range(layers):
+        b = len(descs)
+        src = ("y", b - 1) if b else h
+        qp, qs = random_linear(seed + 10 * l + 1, 5120, hid)
+        op, os_ = random_linear(seed + 10 * l + 2, hid, hid)
+        gp, gs = random_linear(seed + 10 * l + 3, 2 * inter, hid)
+        dp, ds = random_linear(seed + 10 * l + 4, hid, inter)
+        descs += [
+            {"packed": qp, "scales": qs, "x": src, "prologue": fo.PRO_RMSNORM, "eps": 1e-5,
+             "norm": _h(rng.uniform(0.5, 1.5, hid))},
+            {"packed": op, "scales": os_, "x": ("y", b, 0, hid), "residual": src},
+            {"packed": gp, "scales": gs, "x": ("y", b + 1), "prologue": fo.PRO_RMSNORM, "eps": 1e-5,
+             "norm": _h(rng.uniform(0.5, 1.5, hid))},
+            {"packed": dp, "scales": ds, "x": ("y", b + 2), "prologue": fo.PRO_SILU_MUL, "residual": ("y", b + 1)},
+        ]
+    lp, ls = random_linear(seed + 999, vocab, hid)
+    descs.append({"packed": lp, "scales": ls, "x": ("y", len(descs) - 1), "prologue": fo.PRO_RMSNORM, "eps": 1e-5,
+                  "norm": _h(rng.uniform(0.5, 1.5, hid))})
+    return descs
+
+
+def test_persistent_3b_layers_match_per_linear_path(monkeypatch):
+    announce("persistent chain: 3 layers of 3B shapes + 32000-row head, argmax")
+    descs = _layers_3b(500, 3, 32000)
+    (ys_p, am_p), (ys_l, am_l) = _both_paths(descs, monkeypatch, argmax=True)
+    for i, (a, b) in enumerate(zip(ys_p, ys_l)):
+        assert np.isfinite(a.astype(np.float64)).all(), f"linear {i} not finite"
+        _same(a, b, f"linear {i}")
+    assert am_p == am_l
+    # and the first linear against the oracle
+    ref, bound = oracle_linear(descs[0], descs[0]["x"], None)
+    assert fo.fused_within_tolerance(ys_p[0], ref, bound).all()
+
+
+# K values whose rows take each compiled narrow shape: 64 lanes x 1..4 groups,
+# 32 lanes x 1 or 3, 16 lanes x 1 or 3 (and ragged rows below a cover).
+NARROW_K = [32 * g for g in (1, 2, 3, 5, 12, 16, 32, 48, 64, 96, 128, 192, 256, 250, 100)]
+
+
+@pytest.mark.parametrize("seed", [1, 2])
+def test_persistent_random_chains_match_per_linear_path(seed, monkeypatch):
+    """Forty dependent linears of random widths over every narrow shape,
+    random prologues and residuals; consecutive linears share the previous
+    output as x (or its first K entries)."""
+    rng = np.random.default_rng(7000 + seed)
+    dims = [int(rng.choice(NARROW_K))]
+    descs = []
+    x0 = None
+    for i in range(40):
+        k = dims[-1]
+        pro = int(rng.choice([fo.PRO_NONE, fo.PRO_RMSNORM, fo.PRO_SILU_MUL]))
+        n_out = int(rng.choice(NARROW_K))
+        n = 2 * n_out if rng.random() < 0.3 else n_out
+        if pro == fo.PRO_SILU_MUL:
+            # x holds [gate; up] of the previous output: the previous linear is 2K wide
+            pass
+        p, s = random_linear(seed * 1000 + i, n, k)
+        if i == 0:
+            x0 = _h(rng.standard_normal(2 * k if pro == fo.PRO_SILU_MUL else k))
+            x = x0
+        else:
+            prev_n = descs[-1]["packed"].shape[0]
+            need = 2 * k if pro == fo.PRO_SILU_MUL else k
+            if prev_n < need:
+                pro = fo.PRO_NONE
+                need = k
+            if prev_n < need:
+                x = _h(rng.standard_normal(k))
+            else:
+                x = ("y", i - 1, 0, need)
+        d = {"packed": p, "scales": s, "x": x, "prologue": pro, "eps": 1e-5}
+        if pro == fo.PRO_RMSNORM:
+            d["norm"] = _h(rng.uniform(0.5, 1.5, k))
+        if rng.random() < 0.4:
+            d["residual"] = _h(rng.standard_normal(n))
+        descs.append(d)
+        dims.append(n_out if n == n_out else n // 2)
+    announce(f"persistent random chain seed={seed}")
+    (ys_p, _), (ys_l, _) = _both_paths(descs, monkeypatch)
+    for i, (a, b) in enumerate(zip(ys_p, ys_l)):
+        _same(a, b, f"seed {seed} linear {i} ({descs[i]['packed'].shape[0]}x{descs[i]['packed'].shape[1] * 8})")
+
+
+def test_persistent_repeated_and_interleaved_calls(monkeypatch):
+    """The generation numbers continue across launches: the same chain five
+    times, interleaved with another chain, gives the same bits every time."""
+    from paper_2412_15803_amd import wq
+
+    a = _layers_3b(600, 1, 4096)
+    b = _layers_3b(700, 2, 8192)
+    announce("persistent repeated and interleaved chains")
+    monkeypatch.setenv("WQ_FUSED_PERSISTENT", "1")
+    first_a, first_b = run_chain(a)[0], run_chain(b)[0]
+    for rep in range(4):
+        for descs, ref, tag in ((a, first_a, "a"), (b, first_b, "b")):
+            ys, _ = run_chain(descs)
+            for i, (x, y) in enumerate(zip(ys, ref)):
+                _same(x, y, f"chain {tag} rep {rep} linear {i}")
+    wq.wq_fused_check()
+
+
+def test_persistent_timeout_reports_error_and_recovers(monkeypatch):
+    """With the per-wait limit forced to one clock tick from the host, the
+    waits between workgroups run out: every wave still ends, and
+    wq_fused_check reports WQ_ERR_HIP.  The next call with the normal limit
+    gives the right outputs and a clean check."""
+    from paper_2412_15803_amd import wq
+
+    descs = _layers_3b(800, 2, 4096)
+    announce("persistent chain with a one-tick wait limit")
+    monkeypatch.setenv("WQ_FUSED_PERSISTENT", "1")
+    monkeypatch.setenv("WQ_CHAIN_TIMEOUT_TICKS", "1")
+    run_chain(descs)
+    with pytest.raises(wq.WQError) as info:
+        wq.wq_fused_check()
+    assert info.value.status == wq.WQ_ERR_HIP
+    wq.wq_fused_check()  # the condition was cleared by the first check
+    monkeypatch.delenv("WQ_CHAIN_TIMEOUT_TICKS")
+    announce("persistent chain after the timeout")
+    (ys_p, _), (ys_l, _) = _both_paths(descs, monkeypatch)
+    for i, (x, y) in enumerate(zip(ys_p, ys_l)):
+        _same(x, y, f"after timeout linear {i}")
