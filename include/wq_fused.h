@@ -93,22 +93,31 @@ wq_status wq_fused_linears(const wq_fused_linear* linears, int64_t count, int32_
  * How wq_fused_linears runs a chain.  By default each linear is one launch
  * (the per-linear path).  With WQ_FUSED_PERSISTENT=1 in the environment
  * (read at every call), when the current device supports cooperative
- * launches, the stream is not capturing, and every linear's row length is
- * one of the shapes compiled for it (rows of up to 256 groups, K <= 8192,
- * codes below 2 GiB, at most 4096 rows per workgroup), the whole chain is
- * ONE cooperative launch of a persistent kernel instead: one workgroup per
- * CU, a grid-wide barrier between consecutive linears (each workgroup
- * publishes a generation number in a flag of its own and waits for all
- * flags), and the weights of the next linears streamed while the barrier
- * completes.  Its results are bit-identical to the per-linear path.  (It is
- * not the default because on MI355X its barrier costs more than a kernel
- * boundary: see the library's design notes.)  The persistent kernel keeps, per device, a fixed
- * array of workgroup flags and an epoch word in library memory (no
- * allocation), so two chains must not run at the same time on one device.
- * Every wait in it is bounded (half a second per barrier; the environment
+ * launches, the stream is not capturing, the chain has fewer than 32767
+ * linears, every linear's rows are of one of the compiled shapes (up to 256
+ * groups, K <= 8192, codes below 2 GiB, at most 512 rows per wave), every x
+ * and residual is either an input from outside the chain or lies inside the
+ * output of one earlier linear, and no norm weight is an output of the
+ * chain, the chain is instead ONE cooperative launch of a persistent kernel
+ * (one workgroup per CU) followed by a small copy kernel.  Inside it, outputs
+ * pass between workgroups through a library buffer as tagged words, which
+ * the consumers read until the tags show them complete, while the weights
+ * of the next linears keep streaming; the caller's y buffers are written
+ * only by the copy kernel at the end.  Results are bit-identical to the
+ * per-linear path.  (It is not the default: on MI355X a boundary inside it
+ * costs about 5 us, two agent-scope memory round trips, against about
+ * 3.5 us for a kernel boundary of the per-linear path, so a whole 3B-class
+ * token takes longer this way.)
+ *
+ * The persistent path's library memory is part of the resident plan of the
+ * (device, stream) pair (see wq_decode_linears in wq.h): the plan, and 4
+ * bytes per output element of the chain, zeroed when the plan is set up.
+ * Two persistent chains must not run at the same time on one stream's plan.
+ * Every wait in the kernel is bounded (half a second; the environment
  * variable WQ_CHAIN_TIMEOUT_TICKS sets it in clock ticks, for tests): when a
- * wait runs out, every workgroup leaves, that call's outputs are undefined,
- * and the next wq_fused_check reports it.
+ * wait runs out, every later wait of the launch gives up at once, every wave
+ * ends, that call's outputs are undefined, and the next wq_fused_check
+ * reports it.
  */
 wq_status wq_fused_check(void* stream);
 

@@ -98,6 +98,7 @@ struct PlanSlot {
     unsigned char* d = nullptr;
     size_t cap = 0;
     std::vector<unsigned char> bytes;  // the plan the buffer holds
+    size_t extra = 0;                  // zeroed device bytes after it (device-owned state)
     bool frozen = false;
     uint64_t last_use = 0;
 };
@@ -135,6 +136,8 @@ wq_status get_workspace(const char* fn, hipStream_t stream, DecodeWorkspace*& ou
     out = ws;
     return WQ_OK;
 }
+
+size_t align16(size_t v) { return (v + 15) & ~size_t(15); }
 
 size_t pow2_at_least(size_t v) {
     size_t cap = 4096;
@@ -179,10 +182,10 @@ wq_status take_stage(const char* fn, DecodeWorkspace* ws, size_t bytes, Stage*& 
 // on this stream read the old contents).  Under stream capture only a
 // resident plan is accepted, and its slot is frozen.
 wq_status place_plan(const char* fn, DecodeWorkspace* ws, const std::vector<unsigned char>& bytes,
-                     hipStream_t stream, bool capturing, const unsigned char*& d_plan) {
+                     hipStream_t stream, bool capturing, const unsigned char*& d_plan, size_t extra = 0) {
     const uint64_t now = ++ws->clock;
     for (PlanSlot& s : ws->slots) {
-        if (s.bytes == bytes) {
+        if (s.extra == extra && s.bytes == bytes) {
             s.last_use = now;
             if (capturing) s.frozen = true;
             d_plan = s.d;
@@ -205,7 +208,8 @@ wq_status place_plan(const char* fn, DecodeWorkspace* ws, const std::vector<unsi
         slot = &ws->slots.back();
     }
     hipError_t e;
-    if (slot->cap < bytes.size()) {
+    const size_t need = align16(bytes.size()) + extra;
+    if (slot->cap < need) {
         if (slot->d) {
             // Launches queued on this stream may still read the old buffer.
             if ((e = hipStreamSynchronize(stream)) != hipSuccess) return hip_status(fn, e);
@@ -214,7 +218,7 @@ wq_status place_plan(const char* fn, DecodeWorkspace* ws, const std::vector<unsi
         slot->d = nullptr;
         slot->cap = 0;
         slot->bytes.clear();
-        const size_t cap = pow2_at_least(bytes.size());
+        const size_t cap = pow2_at_least(need);
         if ((e = hipMalloc(reinterpret_cast<void**>(&slot->d), cap)) != hipSuccess) return hip_status(fn, e);
         slot->cap = cap;
     }
@@ -225,9 +229,12 @@ wq_status place_plan(const char* fn, DecodeWorkspace* ws, const std::vector<unsi
     if ((e = hipMemcpyAsync(slot->d, st->h, bytes.size(), hipMemcpyHostToDevice, stream)) != hipSuccess)
         return hip_status(fn, e);
     if ((e = hipEventRecord(st->read, stream)) != hipSuccess) return hip_status(fn, e);
+    if (extra && (e = hipMemsetAsync(slot->d + align16(bytes.size()), 0, extra, stream)) != hipSuccess)
+        return hip_status(fn, e);
     st->pending = true;
     st->seq = now;
     slot->bytes = bytes;
+    slot->extra = extra;
     slot->last_use = now;
     d_plan = slot->d;
     return WQ_OK;
@@ -281,15 +288,16 @@ wq_status wq::record_error(wq_status st, const char* message) { return fail(st, 
 
 wq_status wq::hip_error(const char* fn, hipError_t e) { return hip_status(fn, e); }
 
-wq_status wq::resident_plan(const char* fn, hipStream_t stream, const std::vector<unsigned char>& bytes,
-                            const unsigned char*& d_plan, bool& capturing) {
+wq_status wq::resident_plan(const char* fn, hipStream_t stream, const std::vector<unsigned char>& bytes, size_t extra,
+                            const unsigned char*& d_plan, size_t& extra_off, bool& capturing) {
     capturing = false;
+    extra_off = align16(bytes.size());
     wq_status st = capture_state(fn, stream, capturing);
     if (st != WQ_OK) return st;
     std::lock_guard<std::mutex> guard(g_ws_mu);
     DecodeWorkspace* ws = nullptr;
     if ((st = get_workspace(fn, stream, ws)) != WQ_OK) return st;
-    return place_plan(fn, ws, bytes, stream, capturing, d_plan);
+    return place_plan(fn, ws, bytes, stream, capturing, d_plan, extra);
 }
 
 wq_status wq::check_decode_list(const char* fn, const wq_linear* lin, int64_t count, int64_t m, int64_t group,

@@ -22,6 +22,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdlib>
+#include <cstring>
 #include <mutex>
 #include <cstdarg>
 #include <cstdio>
@@ -418,72 +419,79 @@ __global__ __launch_bounds__(kArgThreads) void argmax_kernel(const uint16_t* y, 
 // --------------------------------------------------- persistent dependent chain
 //
 // chain_kernel runs a whole dependent chain (one token's layers) in one
-// cooperative launch: every workgroup stays resident, and the boundary
-// between linear j and j + 1 is a grid-wide barrier instead of a kernel
-// boundary.  What the barrier does not hold up is the weight stream: weights
-// depend on nothing, so each compute wave keeps issuing its next steps --
-// across linear boundaries -- while the barrier and the next prologue run.
+// cooperative launch: every workgroup stays resident, and no kernel
+// boundary separates consecutive linears.  Two things make it pay:
 //
-// Workgroup: seven compute waves and one I/O wave (two waves per SIMD).
-//   * Compute waves own contiguous ranges of each linear's steps (the steps of
-//     all compute waves of the grid, in order, cover the linear), stream them
-//     through two or three register buffers in one sequence across linears,
-//     and leave their rows' fp32 sums in the workgroup's LDS.  At a linear
-//     boundary they only synchronise inside the workgroup, never wait for
-//     their own loads, and then stage the next linear's x_eff exactly as
-//     fused_m1_kernel does (the first four waves run the same prologue code
-//     and order, so the chain's results are bit-identical to one
-//     fused_m1_kernel launch per linear).
-//   * The I/O wave writes the workgroup's rows of y (residual added, one
-//     rounding) with agent-scope stores, waits for them to complete,
-//     publishes the linear's generation number in the workgroup's own flag,
-//     and polls every workgroup's flag with agent-scope loads until all have
-//     reached it, then lets its compute waves go on.
-// Everything one workgroup reads of another's outputs (x, residuals, flags)
-// is read with agent-scope loads, coherent across the chip's L2 caches
-// without invalidating them, so no barrier writes back or invalidates a
-// cache.
+//   * Weights depend on nothing, so each compute wave keeps issuing its next
+//     steps across linear boundaries while it waits for the next x.
+//   * Outputs move between workgroups as data that carries its own
+//     validity: every output row is written to a library buffer T as one
+//     32-bit word (fp16 value, 16-bit tag naming the linear and the launch)
+//     with an agent-scope store, and a consumer reads its x (or residual)
+//     from T with agent-scope loads until every word carries the tag it
+//     expects.  A boundary thus costs a store and a load, not a store, its
+//     acknowledgement, a flag, a poll and then the load.
 //
-// Generation numbers continue across launches (a per-device epoch word read
-// at the start and advanced at the end), so no flag is ever reset and a
-// replayed graph needs no clearing.  Every wait is bounded: a poll that runs
-// past `timeout` clock ticks records the launch in the error words and the
-// workgroup leaves; the others see the error word (or time out) and leave
-// too, so every wave ends.
-constexpr int kChainComputeWaves = 7;
-constexpr int kChainPrologueWaves = kWavesPerBlock;  // the compute waves that stage x_eff (256 threads)
-constexpr int kChainThreads = (kChainComputeWaves + 1) * kWave;
-constexpr int kChainYRows = 4096;     // rows of one linear a workgroup stages
-constexpr int kChainMaxBlocks = 1024;
+// The caller's buffers are written only after the whole chain, by
+// chain_epilogue (the final value of every output element, copied out of
+// T), so no workgroup can overwrite an input that another still reads.
+//
+// Workgroup: eight compute waves (two per SIMD).  They own contiguous ranges
+// of each linear's steps (the ranges of all waves of the grid, in order,
+// cover the linear), stream them through NB register buffers in one
+// sequence across linears, stage their rows' fp32 sums in LDS and write
+// them to T when they move to the next linear.  x_eff of a linear is staged
+// in LDS by the first four waves with fused_m1_kernel's prologue code and
+// order, so results are bit-identical to one fused_m1_kernel launch per
+// linear.  Every wait is bounded: a wait that runs past `timeout` clock
+// ticks records the failure (per chain and in the device's error word) and
+// every later wait of the launch gives up at once, so every wave ends.
+constexpr int kChainWaves = 8;
+constexpr int kChainPrologueWaves = kWavesPerBlock;  // the waves that stage x_eff (256 threads)
+constexpr int kChainThreads = kChainWaves * kWave;
+constexpr int kChainMaxK = 8192;      // rows of up to 256 groups
+constexpr int kChainWaveRows = 512;   // rows of one linear a wave stages
 constexpr uint32_t kChainOut = 0x80000000u;  // offset of unused load slots: past every chain buffer
-
-// Rows per slot of a step: as many as fill `loads` loads.
-__host__ __device__ constexpr int chain_u(int gpl, int loads) { return gpl >= loads ? 1 : loads / gpl; }
-
-// One linear of a chain as the kernel reads it (uploaded once per chain).
-struct ChainLinear {
-    const void* packed;
-    const uint16_t* scales;
-    const uint16_t* x;
-    uint16_t* y;
-    const uint16_t* norm;
-    const uint16_t* residual;
-    int64_t n;
-    int64_t steps;   // ceil(n / rows per step)
-    int32_t ng, lpr, gpl, u;
-    int32_t prologue;
-    float eps;
-};
-static_assert(sizeof(ChainLinear) == 88, "ChainLinear layout");
+constexpr uint32_t kChainTagPeriod = 32767;  // tags 1..32767; 0 marks nothing written
 
 // Cache policy of an agent-scope access (sc1): coherent between the chip's
 // L2 caches, as relaxed agent-scope atomics are.
 constexpr int kCpolAgent = 16;
 
-static __device__ __align__(256) uint32_t chain_flags[kChainMaxBlocks];
-static __device__ uint32_t chain_epoch;
-static __device__ uint32_t chain_err_flag;  // nonzero: the launch with base chain_err_base gave up
-static __device__ uint32_t chain_err_base;
+// Rows per slot of a step: as many as fill `loads` loads.
+__host__ __device__ constexpr int chain_u(int gpl, int loads) { return gpl >= loads ? 1 : loads / gpl; }
+
+// One linear of a chain as the kernel reads it.
+struct ChainLinear {
+    const void* packed;
+    const uint16_t* scales;
+    const uint16_t* x;         // the caller's x, when x_t < 0
+    const uint16_t* norm;
+    const uint16_t* residual;  // the caller's residual, when res_t < 0 (null: none)
+    int64_t n;
+    int64_t steps;             // ceil(n / rows per step)
+    int64_t x_t;               // word offset of x in T (an earlier linear's outputs), or -1
+    int64_t res_t;             // word offset of the residual in T, or -1
+    int64_t y_t;               // word offset of this linear's outputs in T
+    int32_t x_lin, res_lin;    // the linears whose outputs x_t and res_t point into
+    int32_t ng, lpr, gpl, u;
+    int32_t prologue;
+    float eps;
+};
+static_assert(sizeof(ChainLinear) == 112, "ChainLinear layout");
+
+// A run of final output values: T[t, t + count) -> y[0, count).
+struct ChainCopy {
+    uint16_t* y;
+    int64_t t;
+    int64_t count;
+};
+static_assert(sizeof(ChainCopy) == 24, "ChainCopy layout");
+
+// Per-chain control words (in the chain's library buffer, zeroed when the
+// buffer is set up): [0] the launch epoch, [1] epoch + 1 of a launch that
+// gave up.  The device's error word is what wq_fused_check reports.
+static __device__ uint32_t chain_err_flag;
 
 __device__ __forceinline__ uint32_t ld_agent(const uint32_t* p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -492,16 +500,36 @@ __device__ __forceinline__ void st_agent(uint32_t* p, uint32_t v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// First and one-past-last step of compute wave gw (of `waves`) in a linear of
-// `steps` steps.
+__device__ __forceinline__ uint32_t chain_tag(uint32_t epoch, int lin) {
+    return (epoch + (uint32_t)lin) % kChainTagPeriod + 1u;
+}
+
+// First step of compute wave gw (of `waves`) in a linear of `steps` steps.
 __device__ __forceinline__ int64_t chain_step0(int64_t gw, int64_t steps, int64_t waves) { return gw * steps / waves; }
 
+// Bounded waiting, shared by every wait of a launch: gives up once the wait
+// has run past the limit or once any wave of the launch has given up.
+struct ChainWait {
+    uint32_t* ctl;
+    uint32_t epoch;
+    uint64_t timeout;
+    __device__ __forceinline__ bool give_up(uint64_t t0) const {
+        if (ld_agent(ctl + 1) == epoch + 1u) return true;
+        if (__builtin_amdgcn_s_memrealtime() - t0 > timeout) {
+            st_agent(ctl + 1, epoch + 1u);
+            st_agent(&chain_err_flag, 1u);
+            return true;
+        }
+        return false;
+    }
+};
+
 // Issue side: walks the wave's steps in order across linears and issues each
-// step's loads.  Every step issues LOADS code and LOADS scale loads
-// whatever its shape, unused slots pointed past the buffer's end (they
-// return zeros without a memory access), so every path issues the same loads
-// and the compiler's wait counts stay exact.  Past the last linear the loads
-// go to an empty buffer.
+// step's loads.  Every step issues LOADS code and LOADS scale loads whatever
+// its shape, unused slots pointed past the buffer's end (they return zeros
+// without a memory access), so every path issues the same loads and the
+// compiler's wait counts stay exact.  Past the last linear the loads go to
+// an empty buffer.
 struct ChainIssue {
     int lin;          // linear being issued (== count: past the end)
     int64_t step, end;
@@ -591,32 +619,80 @@ __device__ __forceinline__ void chain_compute(const StepBuf& b, const half2v (&x
     }
 }
 
-// x_eff of linear L into LDS by the first 256 compute threads: stage_prologue's
-// loads, reduction order and arithmetic (so x_eff is bit-identical), with
-// PROLOGUE_NONE copying x.  Uses one workgroup barrier, two for RMSNorm; the
-// I/O wave takes the same number.
+// Eight consecutive values of a linear's outputs from T, as one 16-byte
+// chunk of fp16 (two 16-byte loads of tagged words); `ok` when all eight
+// carry `tag`.
+__device__ __forceinline__ u32x4 chain_chunk(const __amdgpu_buffer_rsrc_t& rt, uint32_t word, uint32_t tag, bool& ok) {
+    const u32x4 a = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rt, word * 4u, 0, kCpolAgent));
+    const u32x4 b = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rt, word * 4u + 16u, 0, kCpolAgent));
+    const uint32_t t = tag << 16;
+    ok = ((a.x & 0xFFFF0000u) == t) && ((a.y & 0xFFFF0000u) == t) && ((a.z & 0xFFFF0000u) == t) &&
+         ((a.w & 0xFFFF0000u) == t) && ((b.x & 0xFFFF0000u) == t) && ((b.y & 0xFFFF0000u) == t) &&
+         ((b.z & 0xFFFF0000u) == t) && ((b.w & 0xFFFF0000u) == t);
+    return u32x4{(a.x & 0xFFFFu) | (a.y << 16), (a.z & 0xFFFFu) | (a.w << 16), (b.x & 0xFFFFu) | (b.y << 16),
+                 (b.z & 0xFFFFu) | (b.w << 16)};
+}
+
+// x_eff of linear L into LDS by the first 256 threads: stage_prologue's
+// reduction order and arithmetic (so x_eff is bit-identical), x read either
+// from the caller (external input) or from T, waiting until every word of
+// it carries its producer's tag.  One workgroup barrier, two for RMSNorm;
+// the other waves take the same number.
 template <int CPT>
-__device__ __forceinline__ void chain_prologue(const ChainLinear& L, uint16_t* s_x, float* red) {
+__device__ __forceinline__ void chain_prologue(const ChainLinear& L, const uint32_t* T, uint32_t epoch,
+                                               const ChainWait& w, uint16_t* s_x, float* red) {
     const int tid = threadIdx.x;
     const int chunks = L.ng * (kGroup / 8);
     const bool two = L.prologue != WQ_PROLOGUE_NONE;
-    // x (and the up half) may have been written by other workgroups during
-    // this launch: agent-scope loads, which are coherent across the chip's
-    // caches without invalidating them.  The norm weight is read-only.
-    const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<uint16_t*>(L.x), (short)0, (int)(chunks * 16 * (L.prologue == WQ_PROLOGUE_SILU_MUL ? 2 : 1)),
-        kRawBufferFlags);
-    const WQ_GLOBAL u32x4* ns = gbl(reinterpret_cast<const u32x4*>(L.norm));
+    const bool is_silu = L.prologue == WQ_PROLOGUE_SILU_MUL;
+    const int xchunks = is_silu ? 2 * chunks : chunks;
     u32x4 xa[CPT], xb[CPT];
+    if (L.x_t >= 0) {
+        const __amdgpu_buffer_rsrc_t rt = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint32_t*>(T + L.x_t), (short)0, xchunks * 32, kRawBufferFlags);
+        const uint32_t tag = chain_tag(epoch, L.x_lin);
+        const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+        bool done[CPT];
 #pragma unroll
-    for (int r = 0; r < CPT; ++r) {
-        const int c = tid + r * kBlock;
-        if (c < chunks) {
-            xa[r] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rx, (uint32_t)c * 16u, 0, kCpolAgent));
-            if (L.prologue == WQ_PROLOGUE_RMSNORM) xb[r] = ns[c];
-            else if (two)
-                xb[r] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                                      rx, (uint32_t)(chunks + c) * 16u, 0, kCpolAgent));
+        for (int r = 0; r < CPT; ++r) done[r] = tid + r * kBlock >= chunks;
+        for (;;) {
+            bool all = true;
+#pragma unroll
+            for (int r = 0; r < CPT; ++r) {
+                if (done[r]) continue;
+                const int c = tid + r * kBlock;
+                bool oka = true, okb = true;
+                const u32x4 va = chain_chunk(rt, (uint32_t)c * 8u, tag, oka);
+                u32x4 vb = va;
+                if (is_silu) vb = chain_chunk(rt, (uint32_t)(chunks + c) * 8u, tag, okb);
+                if (oka && okb) {
+                    xa[r] = va;
+                    if (is_silu) xb[r] = vb;
+                    done[r] = true;
+                }
+                all = all && done[r];
+            }
+            if (__all(all)) break;
+            if (w.give_up(t0)) break;
+            __builtin_amdgcn_s_sleep(1);
+        }
+        if (L.prologue == WQ_PROLOGUE_RMSNORM) {
+            const WQ_GLOBAL u32x4* ns = gbl(reinterpret_cast<const u32x4*>(L.norm));
+#pragma unroll
+            for (int r = 0; r < CPT; ++r)
+                if (tid + r * kBlock < chunks) xb[r] = ns[tid + r * kBlock];
+        }
+    } else {
+        const WQ_GLOBAL u32x4* xs = gbl(reinterpret_cast<const u32x4*>(L.x));
+        const WQ_GLOBAL u32x4* bs = L.prologue == WQ_PROLOGUE_RMSNORM ? gbl(reinterpret_cast<const u32x4*>(L.norm))
+                                                                      : xs + chunks;
+#pragma unroll
+        for (int r = 0; r < CPT; ++r) {
+            const int c = tid + r * kBlock;
+            if (c < chunks) {
+                xa[r] = xs[c];
+                if (two) xb[r] = bs[c];
+            }
         }
     }
     float inv = 0.0f;
@@ -625,10 +701,10 @@ __device__ __forceinline__ void chain_prologue(const ChainLinear& L, uint16_t* s
 #pragma unroll
         for (int r = 0; r < CPT; ++r) {
             if (tid + r * kBlock >= chunks) continue;
-            const uint32_t w[4] = {xa[r].x, xa[r].y, xa[r].z, xa[r].w};
+            const uint32_t wv[4] = {xa[r].x, xa[r].y, xa[r].z, xa[r].w};
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const float lo = h2f(w[i] & 0xFFFFu), hi = h2f(w[i] >> 16);
+                const float lo = h2f(wv[i] & 0xFFFFu), hi = h2f(wv[i] >> 16);
                 ss = fmaf(lo, lo, ss);
                 ss = fmaf(hi, hi, ss);
             }
@@ -689,6 +765,39 @@ __device__ __forceinline__ void chain_x(const uint16_t* s_x, int ng, int lpr, in
     }
 }
 
+// Write a wave's staged rows [r0, r1) of linear L to T (residual added, one
+// rounding), tagged as linear `lin` of this launch.
+__device__ __forceinline__ void chain_flush(const ChainLinear& L, int lin, uint32_t* T, uint32_t epoch,
+                                            const ChainWait& w, const float* ylds, int64_t r0, int64_t r1,
+                                            int lane) {
+    wave_lds_sync();
+    const uint32_t tag = chain_tag(epoch, lin) << 16;
+    const uint32_t rtag = L.res_t >= 0 ? chain_tag(epoch, L.res_lin) : 0u;
+    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+    for (int64_t r = r0 + lane; __any(r < r1); r += kWave) {
+        const bool mine = r < r1;
+        float v = mine ? ylds[r - r0] : 0.0f;
+        if (L.res_t >= 0) {
+            // The residual is an earlier linear's output: wait for its tag.
+            uint32_t e = 0;
+            bool ok = !mine;
+            for (;;) {
+                if (!ok) {
+                    e = ld_agent(T + L.res_t + r);
+                    ok = (e >> 16) == rtag;
+                }
+                if (__all(ok) || w.give_up(t0)) break;
+                __builtin_amdgcn_s_sleep(1);
+            }
+            v += h2f(e & 0xFFFFu);
+        } else if (L.residual && mine) {
+            v += h2f(gbl(L.residual)[r]);
+        }
+        if (mine) st_agent(T + L.y_t + r, tag | f2h(v));
+    }
+    wave_lds_sync();
+}
+
 // Step shapes are coded lanes-per-row * 16 + groups-per-lane.  A kernel
 // variant compiles the compute of the shapes in its list only: every extra
 // shape in the dispatch raises the register pressure of all of them.
@@ -701,84 +810,29 @@ __device__ __forceinline__ void chain_compute_any(int shape, const StepBuf& b, c
 }
 
 // A variant: MAXG groups of x per lane (the largest groups-per-lane of its
-// shapes), LOADS code loads per step, NB steps in flight per compute wave,
-// and its shapes S.
+// shapes), LOADS code loads per step, NB steps in flight per wave, and its
+// shapes S.
 template <int MAXG, int LOADS, int NB, int... S>
 __global__ __launch_bounds__(kChainThreads, 2) void chain_kernel(const ChainLinear* __restrict__ plan, int count,
+                                                                 uint32_t* __restrict__ T, uint32_t* ctl,
                                                                  uint64_t timeout) {
-    __shared__ __align__(16) uint16_t s_x[kMaxK];
-    __shared__ __align__(16) float s_y[kChainYRows];
-    __shared__ float s_red[kWavesPerBlock];
-    __shared__ int s_abort;
-    const int lane = threadIdx.x & (kWave - 1);
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-    const int nblocks = gridDim.x;
-    const int64_t waves = (int64_t)nblocks * kChainComputeWaves;
-    const uint32_t base = ld_agent(&chain_epoch);
-
-    if (wave == kChainComputeWaves) {
-        // ------------------------------------------------------------ I/O wave
-        for (int j = 0; j < count; ++j) {
-            const ChainLinear& L = plan[j];
-            if (L.prologue == WQ_PROLOGUE_RMSNORM) __syncthreads();
-            __syncthreads();          // x_eff of j staged
-            __syncthreads();          // the compute waves' rows of j are in LDS
-            // This workgroup's rows of j: those of its four compute waves.
-            const int64_t rows = L.u * (kWave / L.lpr);
-            const int64_t gw0 = (int64_t)blockIdx.x * kChainComputeWaves;
-            const int64_t r0 = chain_step0(gw0, L.steps, waves) * rows;
-            const int64_t r1 = min(L.n, chain_step0(gw0 + kChainComputeWaves, L.steps, waves) * rows);
-            for (int64_t r = r0 + lane; r < r1; r += kWave) {
-                float v = s_y[r - r0];
-                if (L.residual)
-                    v += h2f(__hip_atomic_load(L.residual + r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-                __hip_atomic_store(L.y + r, (uint16_t)f2h(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
-            // Every value another workgroup reads from this launch's outputs
-            // (x, residuals) is written and read with agent-scope accesses,
-            // so publishing needs no cache write-back: the flag goes out once
-            // the stores above have completed.
-            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-            const uint32_t gen = base + (uint32_t)j + 1u;
-            if (lane == 0) st_agent(&chain_flags[blockIdx.x], gen);
-            // Wait for every workgroup's flag to reach gen.
-            const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-            int abort = 0;
-            for (;;) {
-                bool mine = true;
-                for (int b = lane; b < nblocks; b += kWave) mine &= (int32_t)(ld_agent(&chain_flags[b]) - gen) >= 0;
-                if (__all(mine)) break;
-                if (ld_agent(&chain_err_flag) && ld_agent(&chain_err_base) == base) {
-                    abort = 1;
-                    break;
-                }
-                if (__builtin_amdgcn_s_memrealtime() - t0 > timeout) {
-                    if (lane == 0) {
-                        st_agent(&chain_err_base, base);
-                        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-                        st_agent(&chain_err_flag, 1u);
-                    }
-                    abort = 1;
-                    break;
-                }
-                __builtin_amdgcn_s_sleep(1);
-            }
-            // No cache invalidation either: the reads that depend on the flags
-            // are agent-scope loads issued after the flags were seen.
-            asm volatile("" ::: "memory");
-            if (abort && lane == 0) st_agent(&chain_epoch, base + (uint32_t)count);
-            if (lane == 0) s_abort = abort;
-            __syncthreads();          // released: y of j is visible everywhere
-            if (abort) return;
-        }
-        if (blockIdx.x == 0 && lane == 0) st_agent(&chain_epoch, base + (uint32_t)count);
-        return;
-    }
-
-    // ------------------------------------------------------------ compute waves
     static_assert(NB == 2 || NB == 3, "chain pipeline depth");
     static_assert(LOADS <= 8, "a step buffer holds eight loads");
-    const int64_t gw = (int64_t)blockIdx.x * kChainComputeWaves + wave;
+    static_assert(MAXG * kWave * kGroup <= kChainMaxK * 2, "x_eff of the widest row fits its LDS buffer");
+    __shared__ __align__(16) uint16_t s_x[2][kChainMaxK];
+    __shared__ __align__(16) float s_y[kChainWaves][kChainWaveRows];
+    __shared__ float s_red[kWavesPerBlock];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int64_t waves = (int64_t)gridDim.x * kChainWaves;
+    const int64_t gw = (int64_t)blockIdx.x * kChainWaves + wave;
+    ChainWait w;
+    w.ctl = ctl;
+    w.epoch = ld_agent(ctl);
+    w.timeout = timeout;
+    const uint32_t epoch = w.epoch;
+    float* ylds = s_y[wave];
+
     ChainIssue ic;
     ic.lin = 0;
     chain_issue_enter(ic, plan, count, gw, waves, lane);
@@ -793,57 +847,62 @@ __global__ __launch_bounds__(kChainThreads, 2) void chain_kernel(const ChainLine
 
     half2v xr[MAXG][16];
     int cur = -1;            // linear whose x_eff is in xr
-    int64_t r0 = 0;          // first row this workgroup stages for `cur`
     int shape = 0;           // lpr * 16 + gpl of `cur`
-    int ng = 1;
     int64_t n = 0, rows = 1;
-    // Leave linear `cur` (its rows are in LDS) and stage the next one; false
-    // when the I/O wave gave up.
-    auto advance = [&]() __attribute__((always_inline)) -> bool {
-        if (cur >= 0) {
-            __syncthreads();          // rows of cur are in LDS
-            __syncthreads();          // the I/O wave has written them and passed the barrier
-            if (s_abort) return false;
-        }
+    int64_t wr0 = 0, wr1 = 0;  // this wave's rows of `cur`
+    // Leave linear `cur` (write this wave's rows of it to T) and stage the
+    // next one.
+    auto advance = [&]() __attribute__((always_inline)) {
+        if (cur >= 0) chain_flush(plan[cur], cur, T, epoch, w, ylds, wr0, wr1, lane);
         ++cur;
-        if (cur >= count) return true;
+        if (cur >= count) return;
         const ChainLinear& L = plan[cur];
+        uint16_t* sx = s_x[cur & 1];
         if (wave < kChainPrologueWaves) {
-            chain_prologue<MAXG>(L, s_x, s_red);
+            chain_prologue<MAXG>(L, T, epoch, w, sx, s_red);
         } else {
             if (L.prologue == WQ_PROLOGUE_RMSNORM) __syncthreads();
             __syncthreads();
         }
-        ng = L.ng;
         n = L.n;
         rows = L.u * (kWave / L.lpr);
         shape = L.lpr * 16 + L.gpl;
-        r0 = chain_step0((int64_t)blockIdx.x * kChainComputeWaves, L.steps, waves) * rows;
-        chain_x<MAXG>(s_x, ng, L.lpr, L.gpl, lane, xr);
-        return true;
+        wr0 = chain_step0(gw, L.steps, waves) * rows;
+        wr1 = min(n, chain_step0(gw + 1, L.steps, waves) * rows);
+        chain_x<MAXG>(sx, L.ng, L.lpr, L.gpl, lane, xr);
     };
     // Compute the step a buffer holds and refill it with the wave's next
-    // step: 0 to go on, 1 when the wave's steps are done, 2 to leave.
-    auto slot = [&](StepBuf& b, int& lin, int64_t& step) __attribute__((always_inline)) -> int {
-        if (lin >= count) return 1;
-        while (cur < lin)
-            if (!advance()) return 2;
+    // step; false when the wave's steps are done.
+    auto slot = [&](StepBuf& b, int& lin, int64_t& step) __attribute__((always_inline)) -> bool {
+        if (lin >= count) return false;
+        while (cur < lin) advance();
         const int64_t row = step * rows;
         const int nrows = (int)min(rows, n - row);
-        chain_compute_any<MAXG, LOADS, S...>(shape, b, xr, nrows, s_y, (int)(row - r0), lane);
+        chain_compute_any<MAXG, LOADS, S...>(shape, b, xr, nrows, ylds, (int)(row - wr0), lane);
         lin = chain_issue<LOADS>(ic, b, step, plan, count, gw, waves, lane);
-        return 0;
+        return true;
     };
-    int r = 0;
     for (;;) {
-        if ((r = slot(b0, l0, s0)) != 0) break;
-        if ((r = slot(b1, l1, s1)) != 0) break;
+        if (!slot(b0, l0, s0)) break;
+        if (!slot(b1, l1, s1)) break;
         if constexpr (NB == 3)
-            if ((r = slot(b2, l2, s2)) != 0) break;
+            if (!slot(b2, l2, s2)) break;
     }
-    if (r == 2) return;
-    while (cur < count)
-        if (!advance()) return;
+    while (cur < count) advance();
+}
+
+// After a chain: copy the final value of every output element from T to the
+// caller's buffers (runs of T words that no later linear overwrites, so the
+// copies are disjoint), then advance the chain's epoch.
+__global__ __launch_bounds__(256) void chain_epilogue(const ChainCopy* __restrict__ copies, int ncopies,
+                                                      const uint32_t* __restrict__ T, uint32_t* ctl, uint32_t count) {
+    for (int i = blockIdx.x; i < ncopies; i += gridDim.x) {
+        const ChainCopy c = copies[i];
+        const WQ_GLOBAL uint32_t* src = gbl(T + c.t);
+        WQ_GLOBAL uint16_t* dst = gbl(c.y);
+        for (int64_t k = threadIdx.x; k < c.count; k += 256) dst[k] = (uint16_t)(src[k] & 0xFFFFu);
+    }
+    if (blockIdx.x == 0 && threadIdx.x == 0) ctl[0] = ctl[0] + count;
 }
 
 // ------------------------------------------------------------------- host
@@ -982,7 +1041,7 @@ const ChainVariant kChainVariants[] = {
 constexpr int kChainVariantCount = sizeof(kChainVariants) / sizeof(kChainVariants[0]);
 
 // Persistent-chain support of one device: whether cooperative launches work,
-// how many workgroups of each variant are co-resident, the clock rate.
+// how many workgroups of each variant run (one per CU), the clock rate.
 struct ChainDevice {
     bool ready = false;
     bool coop = false;
@@ -1008,9 +1067,7 @@ hipError_t chain_device(int device, ChainDevice*& out) {
             if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kChainVariants[v].fn, kChainThreads, 0)) !=
                 hipSuccess)
                 return e;
-            // One workgroup per CU: its five waves hold two SIMDs' worth of
-            // registers on one of them already.
-            d.blocks[v] = per >= 1 ? std::min(cus, kChainMaxBlocks) : 0;
+            d.blocks[v] = per >= 1 ? cus : 0;
         }
         d.coop = coop != 0;
         d.ticks_per_s = (uint64_t)(rate_khz > 0 ? rate_khz : 100000) * 1000u;
@@ -1030,12 +1087,25 @@ bool env_flag_on(const char* name) {
     return e && e[0] == '1';
 }
 
-// Run the chain as one persistent cooperative launch when every linear fits
-// its limits; `launched` is false (and nothing queued) when the chain must
-// take the per-linear path instead.
+// The latest linear before `j` whose y overlaps [lo, hi): -2 when none does
+// (the span is an input from outside the chain), -1 when the latest one does
+// not hold all of it (not supported), else its index.
+int chain_source(const std::vector<wq_fused_linear>& lin, int j, uintptr_t lo, uintptr_t hi) {
+    for (int i = j - 1; i >= 0; --i) {
+        const uintptr_t ylo = reinterpret_cast<uintptr_t>(lin[i].y), yhi = ylo + 2 * (uintptr_t)lin[i].N;
+        if (ylo < hi && lo < yhi) return (ylo <= lo && hi <= yhi) ? i : -1;
+    }
+    return -2;
+}
+
+// Run the chain as one persistent cooperative launch (and its epilogue)
+// when every linear fits the kernel's limits; `launched` is false (and
+// nothing queued) when the chain must take the per-linear path instead.
 wq_status launch_chain(const char* fn, const std::vector<wq_fused_linear>& lin, hipStream_t stream, bool& launched) {
     launched = false;
     if (!env_flag_on("WQ_FUSED_PERSISTENT")) return WQ_OK;
+    const int count = (int)lin.size();
+    if (count >= (int)kChainTagPeriod) return WQ_OK;
     int device = 0;
     hipError_t e = hipGetDevice(&device);
     if (e != hipSuccess) return err(WQ_ERR_HIP, "%s: HIP error %d (%s)", fn, (int)e, hipGetErrorString(e));
@@ -1055,18 +1125,25 @@ wq_status launch_chain(const char* fn, const std::vector<wq_fused_linear>& lin, 
             const int code = chain_code(lpr, gpl);
             bool found = false;
             for (int k = 0; k < kChainVariants[v].nshapes; ++k) found = found || kChainVariants[v].shapes[k] == code;
-            all = all && found;
+            all = all && found && l.K <= kChainMaxK;
         }
         if (all) variant = v;
     }
     if (variant < 0) return WQ_OK;
     const int loads = kChainVariants[variant].loads;
-    const int blocks = cd->blocks[variant];
+    int blocks = cd->blocks[variant];
     if (blocks < 1) return WQ_OK;
-    const int64_t waves = (int64_t)blocks * kChainComputeWaves;
-    std::vector<unsigned char> bytes(sizeof(ChainLinear) * lin.size());
-    ChainLinear* cl = reinterpret_cast<ChainLinear*>(bytes.data());
-    for (size_t i = 0; i < lin.size(); ++i) {
+    // Tuning override: fewer workgroups than CUs.
+    if (const char* env = std::getenv("WQ_CHAIN_BLOCKS")) {
+        const int b = std::atoi(env);
+        if (b > 0) blocks = std::min(blocks, b);
+    }
+    const int64_t waves = (int64_t)blocks * kChainWaves;
+    // Descriptors: T offsets of every linear's outputs, and where each x and
+    // residual comes from.
+    std::vector<ChainLinear> cl(count);
+    int64_t t_words = 0;
+    for (int i = 0; i < count; ++i) {
         const wq_fused_linear& l = lin[i];
         ChainLinear& c = cl[i];
         int lpr = 64, gpl = 1;
@@ -1076,16 +1153,38 @@ wq_status launch_chain(const char* fn, const std::vector<wq_fused_linear>& lin, 
         const int u = chain_u(gpl, loads);
         const int64_t rows = (int64_t)u * (kWave / lpr);
         const int64_t steps = (l.N + rows - 1) / rows;
-        // Rows a workgroup stages: at most four compute waves' ranges.
-        if (kChainComputeWaves * ((steps + waves - 1) / waves) * rows > kChainYRows) return WQ_OK;
+        if (((steps + waves - 1) / waves) * rows > kChainWaveRows) return WQ_OK;
+        const uintptr_t xlo = reinterpret_cast<uintptr_t>(l.x);
+        const int64_t xk = l.prologue == WQ_PROLOGUE_SILU_MUL ? 2 * l.K : l.K;
+        const int xs = chain_source(lin, i, xlo, xlo + 2 * (uintptr_t)xk);
+        if (xs == -1) return WQ_OK;
+        int rs = -2;
+        if (l.residual) {
+            const uintptr_t rlo = reinterpret_cast<uintptr_t>(l.residual);
+            rs = chain_source(lin, i, rlo, rlo + 2 * (uintptr_t)l.N);
+            if (rs == -1) return WQ_OK;
+        }
+        if (l.prologue == WQ_PROLOGUE_RMSNORM) {
+            // The norm weight must not be an output of the chain.
+            const uintptr_t nlo = reinterpret_cast<uintptr_t>(l.norm_weight);
+            if (chain_source(lin, count, nlo, nlo + 2 * (uintptr_t)l.K) != -2) return WQ_OK;
+        }
+        c = ChainLinear{};
         c.packed = l.packed_w;
         c.scales = l.scales;
         c.x = l.x;
-        c.y = l.y;
         c.norm = l.norm_weight;
         c.residual = l.residual;
         c.n = l.N;
         c.steps = steps;
+        c.y_t = t_words;
+        t_words += l.N;
+        c.x_lin = xs >= 0 ? xs : -1;
+        c.x_t = xs >= 0 ? cl[xs].y_t + (int64_t)((xlo - reinterpret_cast<uintptr_t>(lin[xs].y)) / 2) : -1;
+        c.res_lin = rs >= 0 ? rs : -1;
+        c.res_t = rs >= 0 ? cl[rs].y_t + (int64_t)((reinterpret_cast<uintptr_t>(l.residual) -
+                                                   reinterpret_cast<uintptr_t>(lin[rs].y)) / 2)
+                          : -1;
         c.ng = (int32_t)ng;
         c.lpr = lpr;
         c.gpl = gpl;
@@ -1093,9 +1192,51 @@ wq_status launch_chain(const char* fn, const std::vector<wq_fused_linear>& lin, 
         c.prologue = l.prologue;
         c.eps = l.eps;
     }
+    // Final values: every output element comes from the last linear that
+    // writes it, so the copies of the epilogue are disjoint.
+    std::vector<ChainCopy> copies;
+    {
+        std::vector<Span> claimed;  // sorted, disjoint
+        for (int i = count - 1; i >= 0; --i) {
+            const uintptr_t lo = reinterpret_cast<uintptr_t>(lin[i].y), hi = lo + 2 * (uintptr_t)lin[i].N;
+            uintptr_t p = lo;
+            for (const Span& s : claimed) {
+                if (s.hi <= p || s.lo >= hi) continue;
+                if (s.lo > p) copies.push_back(ChainCopy{reinterpret_cast<uint16_t*>(p), cl[i].y_t + (int64_t)((p - lo) / 2),
+                                                         (int64_t)((s.lo - p) / 2)});
+                p = std::max(p, s.hi);
+            }
+            if (p < hi)
+                copies.push_back(ChainCopy{reinterpret_cast<uint16_t*>(p), cl[i].y_t + (int64_t)((p - lo) / 2),
+                                           (int64_t)((hi - p) / 2)});
+            claimed.push_back(Span{lo, hi});
+            std::sort(claimed.begin(), claimed.end(), [](const Span& a, const Span& b) { return a.lo < b.lo; });
+            std::vector<Span> merged;
+            for (const Span& s : claimed) {
+                if (!merged.empty() && s.lo <= merged.back().hi) merged.back().hi = std::max(merged.back().hi, s.hi);
+                else merged.push_back(s);
+            }
+            claimed.swap(merged);
+        }
+    }
+    {
+        // Runs of at most 4096 values, one workgroup each.
+        std::vector<ChainCopy> split;
+        for (const ChainCopy& c : copies)
+            for (int64_t k = 0; k < c.count; k += 4096)
+                split.push_back(ChainCopy{c.y + k, c.t + k, std::min<int64_t>(4096, c.count - k)});
+        copies.swap(split);
+    }
+    const size_t lin_bytes = sizeof(ChainLinear) * count;
+    std::vector<unsigned char> bytes(lin_bytes + sizeof(ChainCopy) * copies.size());
+    std::memcpy(bytes.data(), cl.data(), lin_bytes);
+    std::memcpy(bytes.data() + lin_bytes, copies.data(), sizeof(ChainCopy) * copies.size());
+    // Zeroed library memory after the plan: the control words, then T.
+    const size_t extra = 16 + (size_t)t_words * 4;
     const unsigned char* d_plan = nullptr;
+    size_t extra_off = 0;
     bool capturing = false;
-    const wq_status st = resident_plan(fn, stream, bytes, d_plan, capturing);
+    const wq_status st = resident_plan(fn, stream, bytes, extra, d_plan, extra_off, capturing);
     // Under stream capture the chain takes the per-linear path: its launches
     // are plain kernel nodes.
     if (capturing) return WQ_OK;
@@ -1106,8 +1247,11 @@ wq_status launch_chain(const char* fn, const std::vector<wq_fused_linear>& lin, 
         if (t > 0) timeout = (uint64_t)t;
     }
     const ChainLinear* plan = reinterpret_cast<const ChainLinear*>(d_plan);
-    int count = (int)lin.size();
-    void* args[] = {&plan, &count, &timeout};
+    const ChainCopy* dcopies = reinterpret_cast<const ChainCopy*>(d_plan + lin_bytes);
+    uint32_t* ctl = reinterpret_cast<uint32_t*>(const_cast<unsigned char*>(d_plan) + extra_off);
+    uint32_t* T = ctl + 4;
+    int cnt = count;
+    void* args[] = {&plan, &cnt, &T, &ctl, &timeout};
     // WQ_CHAIN_COOPERATIVE=0 (for measurements) launches without the
     // co-residency guarantee; the bounded waits still end every wave.
     if (env_flag_off("WQ_CHAIN_COOPERATIVE"))
@@ -1115,6 +1259,11 @@ wq_status launch_chain(const char* fn, const std::vector<wq_fused_linear>& lin, 
     else
         e = hipLaunchCooperativeKernel(kChainVariants[variant].fn, dim3(blocks), dim3(kChainThreads), args, 0, stream);
     if (e != hipSuccess) return err(WQ_ERR_HIP, "%s: HIP error %d (%s)", fn, (int)e, hipGetErrorString(e));
+    const int ncopies = (int)copies.size();
+    hipLaunchKernelGGL(chain_epilogue, dim3((unsigned)std::max(1, std::min(ncopies, 1024))), dim3(256), 0, stream,
+                       dcopies, ncopies, T, ctl, (uint32_t)count);
+    if ((e = hipGetLastError()) != hipSuccess)
+        return err(WQ_ERR_HIP, "%s: HIP error %d (%s)", fn, (int)e, hipGetErrorString(e));
     launched = true;
     return WQ_OK;
 }

@@ -188,11 +188,14 @@ hipError_t launch_groups(const wq_linear* lin, const Group* groups, int ngroups,
 // Place `bytes` in one of the library-owned plan buffers of the current
 // device and `stream` (the resident plans wq_decode_linears keeps, see
 // include/wq.h) and return its device address: no copy when the same bytes
-// are resident already.  Under stream capture only a resident plan is
+// are resident already.  `extra` more bytes of device memory follow the plan
+// at offset `extra_off` (16-byte aligned); they are zeroed when the plan is
+// uploaded and otherwise left as the device last wrote them (state that
+// belongs to this plan).  Under stream capture only a resident plan is
 // accepted, and its buffer is frozen; otherwise WQ_ERR_UNSUPPORTED is
 // returned and nothing is recorded.  `capturing` reports the stream's state.
-wq_status resident_plan(const char* fn, hipStream_t stream, const std::vector<unsigned char>& bytes,
-                        const unsigned char*& d_plan, bool& capturing);
+wq_status resident_plan(const char* fn, hipStream_t stream, const std::vector<unsigned char>& bytes, size_t extra,
+                        const unsigned char*& d_plan, size_t& extra_off, bool& capturing);
 
 // Validation shared by the decode-step entry points (defined with the C ABI):
 // every descriptor as for wq_gemv, and no y overlapping any linear's codes or

@@ -171,3 +171,78 @@ def test_persistent_timeout_reports_error_and_recovers(monkeypatch):
     (ys_p, _), (ys_l, _) = _both_paths(descs, monkeypatch)
     for i, (x, y) in enumerate(zip(ys_p, ys_l)):
         _same(x, y, f"after timeout linear {i}")
+
+
+def _in_place_layers(seed, layers, vocab):
+    """The bench's buffer pattern: one residual stream h updated in place by
+    o and down (residual = y = h), qkv and gate_up outputs reused by every
+    layer, RMSNorm weights per layer; returns a function running the chain
+    from a fresh copy of h0 and returning every buffer and the argmax."""
+    import torch
+
+    from paper_2412_15803_amd import wq
+
+    g = torch.Generator(device="cuda:0")
+    g.manual_seed(seed)
+    hid, inter = 3072, 8192
+    dev = "cuda:0"
+
+    def rnd(shape, lo=None):
+        t = torch.rand(shape, generator=g, device=dev) + 0.5 if lo else torch.randn(shape, generator=g, device=dev)
+        return t.to(torch.float16)
+
+    def lin(n, k):
+        p = torch.randint(-2**31, 2**31 - 1, (n, k // 8), dtype=torch.int32, device=dev, generator=g)
+        s = (torch.rand((n, k // 32), device=dev, generator=g) * 0.01 + 0.001).to(torch.float16)
+        return p, s
+
+    h0 = rnd(hid)
+    h = torch.empty(hid, dtype=torch.float16, device=dev)
+    qkv = torch.empty(5120, dtype=torch.float16, device=dev)
+    gu = torch.empty(2 * inter, dtype=torch.float16, device=dev)
+    logits = torch.empty(vocab, dtype=torch.float16, device=dev)
+    token = torch.empty(1, dtype=torch.int32, device=dev)
+    R, S = wq.PROLOGUE_RMSNORM, wq.PROLOGUE_SILU_MUL
+    chain = []
+    for _ in range(layers):
+        (qp, qs), (op, os_), (gp, gs), (dp, ds) = lin(5120, hid), lin(hid, hid), lin(2 * inter, hid), lin(hid, inter)
+        chain += [dict(packed_w=qp, scales=qs, x=h, y=qkv, prologue=R, norm_weight=rnd(hid, True), eps=1e-5),
+                  dict(packed_w=op, scales=os_, x=qkv[:hid], y=h, residual=h),
+                  dict(packed_w=gp, scales=gs, x=h, y=gu, prologue=R, norm_weight=rnd(hid, True), eps=1e-5),
+                  dict(packed_w=dp, scales=ds, x=gu, y=h, prologue=S, residual=h)]
+    lp, ls = lin(vocab, hid)
+    chain.append(dict(packed_w=lp, scales=ls, x=h, y=logits, prologue=R, norm_weight=rnd(hid, True), eps=1e-5))
+    arr = wq.make_fused_array(chain)
+
+    def run():
+        h.copy_(h0)
+        for t in (qkv, gu, logits):
+            t.fill_(float("nan"))
+        wq.wq_fused_linears(chain, argmax=token, _array=arr)
+        torch.cuda.synchronize()
+        return [t.cpu().numpy().copy() for t in (h, qkv, gu, logits)], int(token.item())
+
+    return run
+
+
+def test_persistent_in_place_residual_stream_matches(monkeypatch):
+    """Outputs written over inputs that other workgroups still read in the
+    same launch (h is read by qkv's and gate_up's prologues and updated in
+    place by o and down): the persistent chain writes the caller's buffers
+    only after the whole chain, and must match the per-linear path."""
+    from paper_2412_15803_amd import wq
+
+    run = _in_place_layers(900, 3, 16000)
+    announce("persistent chain over an in-place residual stream")
+    monkeypatch.setenv("WQ_FUSED_PERSISTENT", "1")
+    bufs_p, tok_p = run()
+    wq.wq_fused_check()
+    bufs_p2, tok_p2 = run()
+    monkeypatch.setenv("WQ_FUSED_PERSISTENT", "0")
+    bufs_l, tok_l = run()
+    monkeypatch.delenv("WQ_FUSED_PERSISTENT", raising=False)
+    for name, a, a2, b in zip(("h", "qkv", "gate_up", "logits"), bufs_p, bufs_p2, bufs_l):
+        assert np.isfinite(b.astype(np.float64)).all(), name
+        _same(a, b, f"in place: {name}")
+        _same(a2, b, f"in place, second call: {name}")
+    assert tok_p == tok_l == tok_p2
