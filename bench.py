@@ -60,6 +60,10 @@ def parse_args():
                     help="with --prefill-only: time only this entry of PREFILL_CONFIGS")
     ap.add_argument("--step-batches", type=str, default=None,
                     help="time only the 3B-class step at these comma-separated batch sizes (for counters)")
+    ap.add_argument("--layers-only", action="store_true",
+                    help="time only the one-call-per-layer figures (for profiling their launches)")
+    ap.add_argument("--stream-only", action="store_true",
+                    help="time only the streaming-read probe")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the per-shape figures (single linears, small batches, 8B-class step)")
     return ap.parse_args()
@@ -373,7 +377,7 @@ def stream_read_ceiling(device, gib=2, calls=10, reps=5):
     from paper_2412_15803_amd import wq
 
     buf = torch.ones(gib << 28, dtype=torch.int32, device=device)
-    sink = torch.zeros(2048, dtype=torch.int32, device=device)
+    sink = torch.zeros(1024, dtype=torch.int32, device=device)
     nbytes = buf.numel() * 4
     wq.stream_read(buf, sink)
     torch.cuda.synchronize()
@@ -916,6 +920,16 @@ def main():
         steps3 = [(lin.n, lin.k) for lin in wl.LLAMA3B_LAYER] * 28 + [(wl.LLAMA3B_LM_HEAD.n, wl.LLAMA3B_LM_HEAD.k)]
         res = time_step_batches(steps3, ms, gen, device, args.steps, args.warmup)
         print(json.dumps({"3B step batches": res}), flush=True)
+        return
+
+    if args.layers_only:
+        log("timing one wq_decode_linears call per layer")
+        print(json.dumps({"layer_calls": layer_configs(device, args.seed)}), flush=True)
+        return
+
+    if args.stream_only:
+        log("timing the streaming-read probe")
+        print(json.dumps({"stream_read_ceiling": stream_read_ceiling(device)}), flush=True)
         return
 
     if args.attention_only:

@@ -264,14 +264,15 @@ wq_status decode_grouped(const char* fn, const wq_linear* lin, int64_t count, in
     DecodeWorkspace* ws = nullptr;
     if ((st = get_workspace(fn, stream, ws)) != WQ_OK) return st;
     const bool matrix = m >= wq::kMatrixCoreMinM && !wq::vector_small_batch();
-    std::vector<unsigned char> bytes(wq::plan::plan_bytes_bound(count));
+    std::vector<unsigned char> bytes(
+        wq::plan::plan_bytes_bound(count, std::max(ws->shape.blocks4, ws->shape.blocks8)));
     PlanBuf pb{bytes.data(), bytes.size(), 0, false};
     std::vector<GroupPlan> gplans(groups.size());
     std::vector<BatchPlan> bplans(groups.size());
     const int64_t target = ws->shape.mb_waves[m <= 2 ? 0 : m <= 4 ? 1 : 2];
     for (size_t i = 0; i < groups.size(); ++i) {
         if (!groups[i].grouped) continue;
-        if (m == 1) gplans[i] = wq::plan::plan_group(lin, groups[i], ws->shape.waves4, ws->shape.waves8, pb);
+        if (m == 1) gplans[i] = wq::plan::plan_group(lin, groups[i], ws->shape.blocks4, ws->shape.blocks8, pb);
         else if (matrix) bplans[i] = wq::plan::plan_batch_group(lin, groups[i], pb);
         else bplans[i] = wq::plan::plan_vector_group(lin, groups[i], target, pb);
     }

@@ -6,15 +6,24 @@
 // reads or overwrites another's data; groups run in stream order, so inside a
 // launch every linear is independent.  Linears are further sorted into shape
 // classes (same lanes per row and groups per lane), each class's rows are cut
-// into steps, and every wave of the grid is given one class and a contiguous,
-// equal share of that class's steps (classes get waves in proportion to
-// their bytes).  A wave therefore streams one long contiguous range of rows,
-// crossing linear boundaries only where its range does, through a loop
-// specialised for its class's shape: two or three register buffers (compute
-// a buffer, refill it with the step that many ahead, go on to the next), so
-// later steps' weights -- of this linear or the next one -- are always in
-// flight while the current step is computed.  Outputs are staged in LDS and
-// written per linear.  No atomics, no waiting between waves.
+// into steps, and every workgroup of the grid is given one class and a
+// contiguous, equal share of that class's steps (classes get workgroups in
+// proportion to their bytes).  A workgroup is one CU's worth of waves (three
+// per SIMD, or two for the wide variant), and its waves share the
+// workgroup's range dynamically: the range is cut into chunks of a few
+// steps, wave w starts on chunk w and then takes the next untaken chunk from
+// a counter in LDS.  Waves that share a SIMD do not run at the same speed
+// (the oldest one wins the issue arbitration: with equal static shares the
+// youngest of three finished 1.6x later than the oldest), so the dynamic
+// share keeps every wave busy until the range is done.  Chunks are taken in
+// order, so a wave's chunks lie close together and it rarely changes linear.
+//
+// Inside a chunk a wave streams its steps through a loop specialised for its
+// class's shape: two to four register buffers (compute a buffer, refill it
+// with the step that many ahead, go on to the next), so later steps' weights
+// -- of this chunk or the next one -- are always in flight while the current
+// step is computed.  Outputs are staged in LDS and written once per run of
+// contiguous rows.  No global atomics, no waiting between workgroups.
 #include "wq_device.h"
 #include "wq_internal.h"
 
@@ -23,78 +32,134 @@ namespace {
 
 using namespace dev;
 
-constexpr int kBlock = 256;
-constexpr int kWavesPerBlock = kBlock / kWave;
+// Waves of one workgroup: what a CU holds of the narrow (MAXG <= 4, three
+// waves per SIMD) and the wide variant (two per SIMD).
+__host__ __device__ constexpr int cu_waves(int maxg) { return maxg <= 4 ? 12 : 8; }
 
-// One step as the pipeline sees it: everything needed to issue and compute
-// it, so the steady state reads no table entries.
+// What computing a step needs (the linear, its rows, its groups per row);
+// issuing it also needs the linear's pointers, which the step iterator holds
+// for the linear it is in.  Steps, rows and step counts are 32-bit: a
+// launch's classes have fewer than 2^31 steps (the host splits larger groups)
+// and a linear read through buffer offsets fewer than 2^28 rows.
 struct Step {
-    int lin;                 // -1 past the end of the wave's range
-    int nrows;               // rows of this step inside its linear
+    int lin;    // -1 once the wave's work is done
+    int nrows;  // rows of this step inside its linear
+    int row;    // first row
     int ng;
+};
+
+// The current linear of a wave's walk.
+struct LinearRef {
+    int lin;
+    int ng;
+    int n;                   // rows, for the last step's row count
     uint32_t scale_bytes;    // n * ng * 2: extent of the scales (codes: 8x)
-    int64_t row;             // first row
     const void* packed;
     const uint16_t* scales;
 };
 
-// Walks the wave's step range [pos, end) of a class: steps are numbered per
-// class in linear order, each linear owning steps [first_step, first_step +
-// steps), so the walk only ever moves forward through the class's list.  The
-// current linear's fields are cached and reloaded only at a boundary.
+// Walks a wave's chunks of one workgroup's share of a class: steps are
+// numbered per class in linear order, each linear owning steps [first_step,
+// first_step + steps); the chunks of one share are taken in increasing
+// order, so within a share the walk only moves forward through the class's
+// list.  The current linear's fields are cached and reloaded only at a
+// boundary.
 struct StepIter {
-    int idx;        // position in the class's linear list
-    int64_t pos;    // next step (class numbering)
-    int64_t end;    // one past the wave's last step
-    int64_t lin_end;  // first step of the next linear
-    Step cur;       // fields of the current linear (row = its first step's row base)
-    int64_t first_step;
+    int idx;          // position in the class's linear list
+    int pos;          // next step (class numbering)
+    int end;          // one past the last step of the current chunk
+    int first_step;   // of the current linear
+    int lin_end;      // first step of the next linear
+    int begin, end_all;  // the workgroup's share of the class
+    int cs;              // its steps per chunk
+    bool done;
+    uint32_t next_chunk;  // the chunk this wave takes next
+    LinearRef cur;
 };
+
+// The next untaken chunk of the workgroup (one LDS atomic, wave-uniform).
+__device__ __forceinline__ uint32_t take_chunk(uint32_t* counter, int lane) {
+    uint32_t v = 0;
+    if (lane == 0) v = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    return __builtin_amdgcn_readfirstlane(v);
+}
 
 __device__ __forceinline__ void load_linear(StepIter& it, const DecodePlan& p, const DecodeClass& c) {
     const int lin = p.class_lin[c.first + it.idx];
     const DecodeEntry& e = p.entries[lin];
     it.cur.lin = lin;
     it.cur.ng = e.ng;
-    it.cur.row = e.n;  // rows of the linear, for the last step's row count
+    it.cur.n = (int)e.n;
     it.cur.packed = e.packed;
     it.cur.scales = e.scales;
     it.cur.scale_bytes = (uint32_t)(e.n * e.ng * 2);
-    it.first_step = e.first_step;
-    it.lin_end = e.first_step + e.steps;
+    it.first_step = (int)e.first_step;
+    it.lin_end = (int)(e.first_step + e.steps);
+}
+
+// Move to the wave's next chunk of the workgroup's share.  Returns false
+// once the share is done.
+__device__ __forceinline__ bool next_chunk(StepIter& it, uint32_t* lds_counter, int lane) {
+    const int64_t start = it.begin + (int64_t)it.next_chunk * it.cs;
+    if (start >= it.end_all) return false;
+    it.pos = (int)start;
+    it.end = min(it.pos + it.cs, it.end_all);
+    it.next_chunk = take_chunk(lds_counter, lane);
+    return true;
 }
 
 template <int R>
-__device__ __forceinline__ Step next_step(StepIter& it, const DecodePlan& p, const DecodeClass& c) {
-    Step s = it.cur;
-    if (it.pos >= it.end) {
+__device__ __forceinline__ Step next_step(StepIter& it, const DecodePlan& p, const DecodeClass& c,
+                                          uint32_t* lds_counter, int lane) {
+    Step s;
+    if (it.pos >= it.end && (it.done || !next_chunk(it, lds_counter, lane))) {
+        it.done = true;  // stay done without taking more chunks
+        it.pos = it.end;
         s.lin = -1;
+        s.nrows = 0;
+        s.row = 0;
+        s.ng = it.cur.ng;
         return s;
     }
+    // Chunks only move forward, so the walk to the chunk's linear does too.
     while (it.pos >= it.lin_end) {
         ++it.idx;
         load_linear(it, p, c);
-        s = it.cur;
     }
-    const int64_t n = it.cur.row;
+    s.lin = it.cur.lin;
+    s.ng = it.cur.ng;
     s.row = (it.pos - it.first_step) * R;
-    s.nrows = (int)min((int64_t)R, n - s.row);
+    s.nrows = min(R, it.cur.n - s.row);
     ++it.pos;
     return s;
 }
 
-// The wave's x registers, the linear they belong to, and the rows of that
-// linear's y staged in LDS ([ybase, yend) of y).  x is switched when the wave
-// computes the first step of another linear: the staged rows of the previous
-// one are written out, and the fresh x loads are the youngest in flight, so
-// the wave waits for its pipeline once per linear it enters.
+// The wave's x registers, the linear they belong to, and a run of
+// contiguous rows of that linear's y staged in LDS ([ybase, yend) of y).
+// The staged rows are written out when the next step's rows do not continue
+// them (a new chunk elsewhere, another linear) or would overflow the slice.
+// x is switched when the wave computes the first step of another linear: the
+// fresh x loads are the youngest in flight, so the wave waits for its
+// pipeline once per linear it enters.
 template <int MAXG>
 struct XSlot {
     half2v xr[MAXG][16];
     int lin;
     uint16_t* y;
-    int64_t ybase, yend;
+    int ybase, yend;
 };
+
+// Write the `count` staged rows ylds[0, count) to y[row0, row0 + count)
+// through a buffer resource (one offset register per lane: this runs while
+// the pipeline's buffers and x are live).
+__device__ __forceinline__ void flush_run(uint16_t* y, int row0, const uint16_t* ylds, int count, int lane) {
+    wave_lds_sync();
+    const __amdgpu_buffer_rsrc_t r =
+        __builtin_amdgcn_make_buffer_rsrc(y + row0, (short)0, count * 2, kRawBufferFlags);
+    for (int i = lane; i < count; i += kWave)
+        __builtin_amdgcn_raw_buffer_store_b16(ylds[i], r, (uint32_t)i * 2u, 0, 0);
+    wave_lds_sync();  // stores have read the slice before it is refilled
+}
 
 // x and y of the linear a step belongs to are read from the plan only when
 // the wave enters that linear.
@@ -102,24 +167,27 @@ template <int LPR, int GPL, int MAXG>
 __device__ __forceinline__ void compute_from(const StepBuf& b, XSlot<MAXG>& xs, const Step& s,
                                              const DecodePlan& p, uint16_t* ylds, int lane) {
     if (s.lin < 0) return;
-    if (xs.lin != s.lin) {
-        if (xs.lin >= 0) flush_y(xs.y, xs.ybase, ylds, (int)(xs.yend - xs.ybase), lane);
-        const DecodeEntry& e = p.entries[s.lin];
-        load_x_lane<LPR, GPL, MAXG>(e.x, s.ng, lane, xs.xr);
-        xs.lin = s.lin;
-        xs.y = e.y;
+    const bool new_lin = xs.lin != s.lin;
+    if (new_lin || s.row != xs.yend || s.row + s.nrows - xs.ybase > kYRows) {
+        if (xs.lin >= 0) flush_run(xs.y, xs.ybase, ylds, xs.yend - xs.ybase, lane);
+        if (new_lin) {
+            const DecodeEntry& e = p.entries[s.lin];
+            load_x_lane<LPR, GPL, MAXG>(e.x, s.ng, lane, xs.xr);
+            xs.lin = s.lin;
+            xs.y = e.y;
+        }
         xs.ybase = s.row;
     }
-    compute_step<LPR, GPL, MAXG>(b, xs.xr, s.nrows, ylds, (int)(s.row - xs.ybase), lane);
+    compute_step<LPR, GPL, MAXG>(b, xs.xr, s.nrows, ylds, s.row - xs.ybase, lane);
     xs.yend = s.row + s.nrows;
 }
 
-// Issues are unconditional: past the end of the range the wave re-loads its
-// last valid step (never computed), so every path through the loop issues
-// the same loads and the compiler's wait counts stay exact.
+// Issues are unconditional: once the wave's work is done it re-loads row 0
+// of its current linear (never computed), so every path through the loop
+// issues the same loads and the compiler's wait counts stay exact.
 template <int LPR, int GPL>
-__device__ __forceinline__ void issue_from(StepBuf& b, const Step& s, int lane) {
-    issue_step<LPR, GPL, kCpolNonTemporal>(b, make_rsrc(s.packed, s.scales, s.scale_bytes), s.row, s.ng, lane);
+__device__ __forceinline__ void issue_from(StepBuf& b, const Step& s, const LinearRef& l, int lane) {
+    issue_step<LPR, GPL, kCpolNonTemporal>(b, make_rsrc(l.packed, l.scales, l.scale_bytes), s.row, l.ng, lane);
 }
 
 // Register buffers in the pipeline: as many steps as fit a budget of
@@ -139,24 +207,35 @@ constexpr int pipeline_depth() {
     return nb < 2 ? 2 : (nb > 4 ? 4 : nb);
 }
 
-// The plan keeps every wave's range at most kYRows / R steps, so the staged
-// rows of one linear always fit the wave's LDS slice.
+// Steps per chunk: up to twice the pipeline depth (a wave's loads of the
+// next chunk are then issued while half of the current one is still to be
+// computed), fewer when the workgroup's range would give some of its waves
+// no chunk at all.
 template <int LPR, int GPL, int MAXG>
-__device__ __forceinline__ void run_range(const DecodePlan& p, const DecodeClass& c, int64_t begin, int64_t end,
-                                          uint16_t* ylds, int lane) {
-    constexpr int R = StepShape<LPR, GPL>::ROWS;
+__device__ __forceinline__ int chunk_steps(int range, int waves) {
+    constexpr int kMax = 2 * pipeline_depth<LPR, GPL, MAXG>();
+    return max(1, min(kMax, range / waves));
+}
+
+// One wave's share of its workgroup's steps: chunk `wave` first, then
+// whatever chunk the counter hands out next.
+template <int LPR, int GPL, int MAXG>
+__device__ __forceinline__ void run_block(const DecodePlan& p, const DecodeClass& c, const DecodeBlock& b,
+                                          uint32_t* lds_counter, int wave, int waves, uint16_t* ylds, int lane) {
     constexpr int NB = pipeline_depth<LPR, GPL, MAXG>();
+    constexpr int R = StepShape<LPR, GPL>::ROWS;
+    static_assert(2 * NB * R <= kYRows, "a chunk's rows fit the wave's staging slice");
     StepIter it;
-    it.pos = begin;
-    it.end = end;
-    // Find the linear holding step `begin` (the class lists are short, a
-    // forward scan is enough).
-    it.idx = 0;
+    it.begin = b.begin;
+    it.end_all = b.end;
+    it.cs = chunk_steps<LPR, GPL, MAXG>(b.end - b.begin, waves);
+    it.done = false;
+    it.next_chunk = (uint32_t)wave;
+    if (!next_chunk(it, lds_counter, lane)) return;  // fewer chunks than waves
+    // The linear holding the workgroup's first step comes with the plan; the
+    // wave's first chunk is at most a few steps further.
+    it.idx = b.pos;
     load_linear(it, p, c);
-    while (begin >= it.lin_end) {
-        ++it.idx;
-        load_linear(it, p, c);
-    }
     XSlot<MAXG> xs;
     xs.lin = -1;
     xs.y = nullptr;
@@ -167,20 +246,18 @@ __device__ __forceinline__ void run_range(const DecodePlan& p, const DecodeClass
     for (int i = 0; i < NB; ++i) st[i].lin = -1;
     // The first pass only issues; afterwards each pass computes the step a
     // buffer holds and refills that buffer with the wave's next step.
-    Step last = it.cur;  // the latest valid step (the range is never empty)
     for (;;) {
         bool any = false;
 #pragma unroll
         for (int i = 0; i < NB; ++i) {
             compute_from<LPR, GPL, MAXG>(buf[i], xs, st[i], p, ylds, lane);
-            st[i] = next_step<R>(it, p, c);
-            if (st[i].lin >= 0) last = st[i];
+            st[i] = next_step<R>(it, p, c, lds_counter, lane);
             any = any || st[i].lin >= 0;
-            issue_from<LPR, GPL>(buf[i], st[i].lin >= 0 ? st[i] : last, lane);
+            issue_from<LPR, GPL>(buf[i], st[i], it.cur, lane);
         }
         if (!any) break;
     }
-    if (xs.lin >= 0) flush_y(xs.y, xs.ybase, ylds, (int)(xs.yend - xs.ybase), lane);
+    if (xs.lin >= 0) flush_run(xs.y, xs.ybase, ylds, xs.yend - xs.ybase, lane);
 }
 
 // The (lanes per row, groups per lane) shapes a launch supports: those with
@@ -189,35 +266,39 @@ __device__ __forceinline__ void run_range(const DecodePlan& p, const DecodeClass
 #define WQ_SHAPES_8(X) WQ_SHAPES_4(X) X(64, 5) X(64, 6) X(64, 7) X(64, 8) X(32, 5) X(32, 7) X(16, 5) X(16, 7)
 
 // The plan arrays arrive as separate read-only, non-aliasing arguments, so
-// every table read is a scalar load with a wave-uniform value.
-// Three waves per SIMD fit the narrow variant without spilling; the wide
-// one (up to eight groups of x per lane) stays at two.
+// every table read is a scalar load with a wave-uniform value.  One
+// workgroup per CU: three waves per SIMD fit the narrow variant without
+// spilling, the wide one (up to eight groups of x per lane) stays at two.
 template <int MAXG>
-__global__ __launch_bounds__(kBlock, MAXG <= 4 ? 3 : 2) void grouped_m1_kernel(const DecodeEntry* __restrict__ entries,
-                                                            const DecodeClass* __restrict__ classes,
-                                                            const int32_t* __restrict__ class_lin, int nclasses) {
+__global__ __launch_bounds__(cu_waves(MAXG) * kWave, cu_waves(MAXG) / 4) void grouped_m1_kernel(
+    const DecodeEntry* __restrict__ entries, const DecodeClass* __restrict__ classes,
+    const int32_t* __restrict__ class_lin, const DecodeBlock* __restrict__ blocks, int nclasses) {
+    constexpr int kWaves = cu_waves(MAXG);
+    __shared__ __align__(16) uint16_t s_y[kWaves][kYRows];
+    __shared__ uint32_t s_chunk;
+    if (threadIdx.x == 0) s_chunk = kWaves;  // chunks 0 .. kWaves - 1 are the waves' first
+    __syncthreads();
     DecodePlan p;
     p.entries = entries;
     p.classes = classes;
     p.class_lin = class_lin;
+    p.blocks = blocks;
     p.nclasses = nclasses;
     const int lane = threadIdx.x & (kWave - 1);
     // The wave index is the same in every lane; saying so keeps everything
     // derived from it in scalar registers and all branches uniform.
-    const int wave = __builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerBlock + threadIdx.x / kWave);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int blk = blockIdx.x;
     int ci = -1;
     for (int k = 0; k < nclasses; ++k)
-        if (classes[k].waves_begin <= wave && wave < classes[k].waves_begin + classes[k].waves) ci = k;
+        if (classes[k].blocks_begin <= blk && blk < classes[k].blocks_begin + classes[k].blocks) ci = k;
     if (ci < 0) return;
     const DecodeClass& c = classes[ci];
-    const int64_t i = wave - c.waves_begin;
-    const int64_t begin = i * c.steps / c.waves;
-    const int64_t end = (i + 1) * c.steps / c.waves;
-    if (begin >= end) return;
-    __shared__ __align__(16) uint16_t s_y[kWavesPerBlock][kYRows];
-    uint16_t* ylds = s_y[threadIdx.x / kWave];
+    const DecodeBlock& b = blocks[blk];
+    if (b.begin >= b.end) return;
+    uint16_t* ylds = s_y[wave];
 #define WQ_RUN(L, G) \
-    if (c.lpr == L && c.gpl == G) { run_range<L, G, MAXG>(p, c, begin, end, ylds, lane); return; }
+    if (c.lpr == L && c.gpl == G) { run_block<L, G, MAXG>(p, c, b, &s_chunk, wave, kWaves, ylds, lane); return; }
     if constexpr (MAXG <= 4) {
         WQ_SHAPES_4(WQ_RUN)
     } else {
@@ -228,28 +309,27 @@ __global__ __launch_bounds__(kBlock, MAXG <= 4 ? 3 : 2) void grouped_m1_kernel(c
 
 }  // namespace
 
-hipError_t launch_grouped_m1(const DecodePlan& plan, int max_gpl, int waves, hipStream_t stream) {
-    const int blocks = (waves + kWavesPerBlock - 1) / kWavesPerBlock;
+hipError_t launch_grouped_m1(const DecodePlan& plan, int max_gpl, int blocks, hipStream_t stream) {
     if (max_gpl <= 4) {
-        hipLaunchKernelGGL((grouped_m1_kernel<4>), dim3(blocks), dim3(kBlock), 0, stream, plan.entries,
-                           plan.classes, plan.class_lin, plan.nclasses);
+        hipLaunchKernelGGL((grouped_m1_kernel<4>), dim3(blocks), dim3(cu_waves(4) * kWave), 0, stream,
+                           plan.entries, plan.classes, plan.class_lin, plan.blocks, plan.nclasses);
     } else {
-        hipLaunchKernelGGL((grouped_m1_kernel<8>), dim3(blocks), dim3(kBlock), 0, stream, plan.entries,
-                           plan.classes, plan.class_lin, plan.nclasses);
+        hipLaunchKernelGGL((grouped_m1_kernel<8>), dim3(blocks), dim3(cu_waves(8) * kWave), 0, stream,
+                           plan.entries, plan.classes, plan.class_lin, plan.blocks, plan.nclasses);
     }
     return hipGetLastError();
 }
 
-hipError_t grouped_capacity(int max_gpl, int device, int& waves) {
+hipError_t grouped_capacity(int max_gpl, int device, int& blocks) {
     int per_cu = 0, cus = 0;
     hipError_t e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device);
     if (e != hipSuccess) return e;
     if (max_gpl <= 4)
-        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, grouped_m1_kernel<4>, kBlock, 0);
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, grouped_m1_kernel<4>, cu_waves(4) * kWave, 0);
     else
-        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, grouped_m1_kernel<8>, kBlock, 0);
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, grouped_m1_kernel<8>, cu_waves(8) * kWave, 0);
     if (e != hipSuccess) return e;
-    waves = (per_cu > 0 ? per_cu : 1) * (cus > 0 ? cus : 1) * kWavesPerBlock;
+    blocks = (per_cu > 0 ? per_cu : 1) * (cus > 0 ? cus : 1);
     return hipSuccess;
 }
 

@@ -66,24 +66,36 @@ struct DecodeEntry {
 static_assert(sizeof(DecodeEntry) == 72, "DecodeEntry layout");
 
 // Linears of one launch with the same step shape.  The class's steps are
-// split into `waves` equal contiguous ranges, one per wave, for the waves
-// [waves_begin, waves_begin + waves) of the grid.
+// split into `blocks` equal contiguous ranges, one per workgroup, for the
+// workgroups [blocks_begin, blocks_begin + blocks) of the grid.
 struct DecodeClass {
     int32_t lpr, gpl;     // the class's step shape
     int32_t first;        // offset of its linears in the class list
     int32_t count;        // number of linears
     int64_t steps;        // steps over all its linears
-    int32_t waves_begin;
-    int32_t waves;
+    int32_t blocks_begin;
+    int32_t blocks;
 };
 static_assert(sizeof(DecodeClass) == 32, "DecodeClass layout");
 
+// One workgroup's share of its class in a grouped launch: steps [begin,
+// end) of the class's numbering, and the position (in the class's list) of
+// the linear that holds step `begin`.
+struct DecodeBlock {
+    int32_t pos;
+    int32_t begin, end;
+    int32_t pad;
+};
+static_assert(sizeof(DecodeBlock) == 16, "DecodeBlock layout");
+
 // Device-side view of one grouped launch: the entries, the class
-// descriptors and, per class, the indices of its linears in order.
+// descriptors, per class the indices of its linears in order, and per
+// workgroup its share.
 struct DecodePlan {
     const DecodeEntry* entries;
     const DecodeClass* classes;
     const int32_t* class_lin;
+    const DecodeBlock* blocks;
     int32_t nclasses;
 };
 
@@ -119,11 +131,13 @@ __host__ __device__ inline int64_t mb_padded_groups(int64_t ng) {
 constexpr int kDecodeMaxGpl = 8;
 constexpr int kMaxClasses = 16;
 
-// Launch the grouped batch-1 GEMV over a plan in device memory with `waves`
-// waves (the sum of the classes' waves).
-hipError_t launch_grouped_m1(const DecodePlan& plan, int max_gpl, int waves, hipStream_t stream);
+// Launch the grouped batch-1 GEMV over a plan in device memory with
+// `blocks` workgroups (the sum of the classes' workgroups), each one CU's
+// worth of waves.
+hipError_t launch_grouped_m1(const DecodePlan& plan, int max_gpl, int blocks, hipStream_t stream);
 
-// Waves of the grouped kernel (for max_gpl) that the device holds at once.
-hipError_t grouped_capacity(int max_gpl, int device, int& waves);
+// Workgroups of the grouped kernel (for max_gpl) that the device holds at
+// once: one per CU.
+hipError_t grouped_capacity(int max_gpl, int device, int& blocks);
 
 }  // namespace wq

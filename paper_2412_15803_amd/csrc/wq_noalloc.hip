@@ -160,7 +160,7 @@ extern "C" wq_status wq_decode_linears_noalloc(const wq_linear* linears, int64_t
     PlanBuf pb{g_plan, kScratchBytes, 0, false};
     for (int i = 0; i < ngroups; ++i) {
         if (!g_groups[i].grouped) continue;
-        if (M == 1) g_gplans[i] = plan::plan_group(linears, g_groups[i], ds->shape.waves4, ds->shape.waves8, pb);
+        if (M == 1) g_gplans[i] = plan::plan_group(linears, g_groups[i], ds->shape.blocks4, ds->shape.blocks8, pb);
         else if (matrix) g_bplans[i] = plan::plan_batch_group(linears, g_groups[i], pb);
         else g_bplans[i] = plan::plan_vector_group(linears, g_groups[i], target, pb);
     }

@@ -88,15 +88,21 @@ struct Group {
     bool grouped;  // run with a grouped kernel (else one GEMV launch per linear)
 };
 
+// Rows of one group at most: the grouped kernels number a launch's steps
+// (at most one per row) in 32-bit integers.
+constexpr int64_t kGroupMaxRows = int64_t(1) << 30;
+
 // Split linears[0, count) into consecutive groups in which no linear reads the
 // output of, or writes the input or output of, another linear of the same
 // group.  Groups run in stream order, so this reproduces running the linears
 // one after another.  Linears the grouped kernels cannot take (K > 16384 at
-// M = 1, or codes of 4 GiB or more) form groups of their own.  Calls
-// emit(Group) in order; `reads` and `writes` are empty dependency sets.
+// M = 1, or codes of 4 GiB or more) form groups of their own, and a group
+// closes before its rows would pass kGroupMaxRows.  Calls emit(Group) in
+// order; `reads` and `writes` are empty dependency sets.
 template <class Deps, class Emit>
 void split_groups(const wq_linear* lin, int count, int64_t m, Deps& reads, Deps& writes, Emit emit) {
     int begin = 0;
+    int64_t rows = 0;
     for (int i = 0; i < count; ++i) {
         const wq_linear& l = lin[i];
         const bool too_long = m == 1 && l.K / 32 > 64 * kDecodeMaxGpl;
@@ -106,17 +112,20 @@ void split_groups(const wq_linear* lin, int count, int64_t m, Deps& reads, Deps&
             reads.clear();
             writes.clear();
             begin = i + 1;
+            rows = 0;
             continue;
         }
         const Span x = span_of(l.x, 2 * m * l.K), y = span_of(l.y, 2 * m * l.N);
-        if (i > begin && (writes.hits(x) || reads.hits(y) || writes.hits(y))) {
+        if (i > begin && (writes.hits(x) || reads.hits(y) || writes.hits(y) || rows + l.N > kGroupMaxRows)) {
             emit(Group{begin, i, true});
             reads.clear();
             writes.clear();
             begin = i;
+            rows = 0;
         }
         reads.add(x);
         writes.add(y);
+        rows += l.N;
     }
     if (begin < count) emit(Group{begin, count, true});
 }
@@ -131,18 +140,19 @@ struct PlanBuf {
 };
 
 // Bytes of the plans of `count` linears in any grouping, for sizing a
-// PlanBuf: per group at most entries + classes + class list, each 16-byte
-// aligned.
-inline size_t plan_bytes_bound(int64_t count) {
-    return (size_t)count * (sizeof(DecodeEntry) + sizeof(int32_t) + 48 + sizeof(DecodeClass) * kMaxClasses);
+// PlanBuf: per group at most entries + classes + class list + the shares of
+// at most `max_blocks` + kMaxClasses workgroups, each 16-byte aligned.
+inline size_t plan_bytes_bound(int64_t count, int max_blocks) {
+    return (size_t)count * (sizeof(DecodeEntry) + sizeof(int32_t) + 80 + sizeof(DecodeClass) * kMaxClasses +
+                            sizeof(DecodeBlock) * ((size_t)max_blocks + kMaxClasses));
 }
 
 // Plan of one batch-1 grouped launch: offsets into the plan bytes.
 struct GroupPlan {
-    size_t off_entries, off_classes, off_list;
+    size_t off_entries, off_classes, off_list, off_blocks;
     int nclasses;
     int max_gpl;
-    int waves;
+    int blocks;
 };
 
 // Plan of one small-batch grouped launch: entries, each owning a run of
@@ -155,8 +165,8 @@ struct BatchPlan {
 };
 
 // Append the batch-1 plan of linears [g.begin, g.end); `capacity4` and
-// `capacity8` are the waves the device holds at once of the narrow and wide
-// grouped kernels.
+// `capacity8` are the workgroups the device holds at once of the narrow and
+// wide grouped kernels.
 GroupPlan plan_group(const wq_linear* lin, const Group& g, int capacity4, int capacity8, PlanBuf& out);
 
 // Append the matrix-core (M >= 8) plan of a group.
@@ -167,12 +177,12 @@ BatchPlan plan_vector_group(const wq_linear* lin, const Group& g, int64_t target
 
 // The device's resident-wave capacities the planners need.
 struct DeviceShape {
-    int waves4 = 0, waves8 = 0;       // grouped batch-1 kernel, narrow and wide variants
+    int blocks4 = 0, blocks8 = 0;     // grouped batch-1 kernel, narrow and wide variants
     int64_t mb_waves[3] = {0, 0, 0};  // vector small-batch target waves for m <= 2, 4, 8
 };
 
 // Query `device` (hipOccupancy* and attributes, no allocation) and apply the
-// WQ_GROUPED_WAVES and WQ_MB_WAVES tuning overrides.
+// WQ_GROUPED_BLOCKS and WQ_MB_WAVES tuning overrides.
 hipError_t device_shape(int device, DeviceShape& out);
 
 // Launch one call's planned groups in order on `stream`.  `d_plan` is the

@@ -33,9 +33,15 @@ int class_of(const DecodeClass* cls, int ncls, int lpr, int gpl) {
 
 }  // namespace
 
-// Classes (linears of one step shape) get waves in proportion to their
-// bytes, at least one and at most one per step; every wave then streams one
-// contiguous range of its class's steps.
+// What a row costs beyond its bytes (its reduction and output), in bytes of
+// streaming: measured on the 3B-class step, whose K = 3072 rows (1728 bytes)
+// took about 8% longer per byte than its K = 8192 rows (4608 bytes) when
+// workgroups were split by bytes alone.
+constexpr double kRowCost = 256.0;
+
+// Classes (linears of one step shape) get workgroups in proportion to their
+// bytes plus kRowCost per row, at least one and at most one per step; every
+// workgroup then streams one contiguous range of its class's steps.
 GroupPlan plan_group(const wq_linear* lin, const Group& g, int capacity4, int capacity8, PlanBuf& out) {
     const int count = g.end - g.begin;
     GroupPlan gp{};
@@ -56,14 +62,28 @@ GroupPlan plan_group(const wq_linear* lin, const Group& g, int capacity4, int ca
         const int r = rows_per_step(lpr, gpl);
         cls[c].steps += (l.N + r - 1) / r;
         cls[c].count += 1;
-        work[c] += (double)l.N * (double)(l.K / 2 + l.K / 16);
+        work[c] += (double)l.N * ((double)(l.K / 2 + l.K / 16) + kRowCost);
     }
     gp.nclasses = ncls;
     gp.max_gpl = max_gpl;
     gp.off_entries = align16(out.size);
     gp.off_classes = align16(gp.off_entries + sizeof(DecodeEntry) * count);
     gp.off_list = align16(gp.off_classes + sizeof(DecodeClass) * ncls);
-    const size_t end = align16(gp.off_list + sizeof(int32_t) * count);
+    const int capacity = max_gpl <= 4 ? capacity4 : capacity8;
+    double total = 0.0;
+    for (int c = 0; c < ncls; ++c) total += work[c];
+    int blocks = 0, off = 0;
+    for (int c = 0; c < ncls; ++c) {
+        int64_t bc = (int64_t)(capacity * work[c] / total);
+        bc = std::max<int64_t>(1, std::min<int64_t>(bc, cls[c].steps));
+        cls[c].blocks_begin = blocks;
+        cls[c].blocks = (int32_t)bc;
+        blocks += (int)bc;
+        cls[c].first = off;
+        off += cls[c].count;
+    }
+    gp.off_blocks = align16(gp.off_list + sizeof(int32_t) * count);
+    const size_t end = align16(gp.off_blocks + sizeof(DecodeBlock) * blocks);
     if (out.overflow || end > out.cap) {
         out.overflow = true;
         return gp;
@@ -71,24 +91,6 @@ GroupPlan plan_group(const wq_linear* lin, const Group& g, int capacity4, int ca
     std::memset(out.data + out.size, 0, end - out.size);
     DecodeEntry* ents = reinterpret_cast<DecodeEntry*>(out.data + gp.off_entries);
     int32_t* list = reinterpret_cast<int32_t*>(out.data + gp.off_list);
-    const int capacity = max_gpl <= 4 ? capacity4 : capacity8;
-    double total = 0.0;
-    for (int c = 0; c < ncls; ++c) total += work[c];
-    int waves = 0, off = 0;
-    for (int c = 0; c < ncls; ++c) {
-        int64_t wc = (int64_t)(capacity * work[c] / total);
-        wc = std::max<int64_t>(1, std::min<int64_t>(wc, cls[c].steps));
-        // A wave stages at most kYRows rows of y: at most that many rows' worth
-        // of steps per wave, even if the class then gets more waves than its
-        // share of the device.
-        const int64_t max_steps = dev::kYRows / rows_per_step(cls[c].lpr, cls[c].gpl);
-        wc = std::max<int64_t>(wc, (cls[c].steps + max_steps - 1) / max_steps);
-        cls[c].waves_begin = waves;
-        cls[c].waves = (int32_t)wc;
-        waves += (int)wc;
-        cls[c].first = off;
-        off += cls[c].count;
-    }
     // Entries in list order, each with its first step in its class's
     // numbering; the class lists name the linears of a class in order.
     int64_t next_step[kMaxClasses] = {};
@@ -108,8 +110,27 @@ GroupPlan plan_group(const wq_linear* lin, const Group& g, int capacity4, int ca
         next_step[c] += e.steps;
         list[cls[c].first + filled[c]++] = i;
     }
+    // Per workgroup, its equal share of its class's steps and the list
+    // position of the linear holding the share's first step (the workgroups
+    // of a class start at increasing steps).
+    DecodeBlock* blk = reinterpret_cast<DecodeBlock*>(out.data + gp.off_blocks);
+    for (int c = 0; c < ncls; ++c) {
+        int k = 0;
+        for (int j = 0; j < cls[c].blocks; ++j) {
+            const int64_t first = (int64_t)j * cls[c].steps / cls[c].blocks;
+            while (k + 1 < cls[c].count) {
+                const DecodeEntry& e = ents[list[cls[c].first + k]];
+                if (first < e.first_step + e.steps) break;
+                ++k;
+            }
+            DecodeBlock& b = blk[cls[c].blocks_begin + j];
+            b.pos = k;
+            b.begin = (int32_t)first;
+            b.end = (int32_t)((int64_t)(j + 1) * cls[c].steps / cls[c].blocks);
+        }
+    }
     std::memcpy(out.data + gp.off_classes, cls, sizeof(DecodeClass) * ncls);
-    gp.waves = waves;
+    gp.blocks = blocks;
     out.size = end;
     return gp;
 }
@@ -182,17 +203,17 @@ BatchPlan plan_vector_group(const wq_linear* lin, const Group& g, int64_t target
 
 hipError_t device_shape(int device, DeviceShape& out) {
     hipError_t e;
-    if ((e = grouped_capacity(4, device, out.waves4)) != hipSuccess) return e;
-    if ((e = grouped_capacity(8, device, out.waves8)) != hipSuccess) return e;
+    if ((e = grouped_capacity(4, device, out.blocks4)) != hipSuccess) return e;
+    if ((e = grouped_capacity(8, device, out.blocks8)) != hipSuccess) return e;
     for (int i = 0; i < 3; ++i)
         if ((e = mb_target_waves(2 << i, device, out.mb_waves[i])) != hipSuccess) return e;
-    // Tuning override: fewer waves than the device holds (never more, since
-    // every wave owns a fixed share of the work).
-    if (const char* env = std::getenv("WQ_GROUPED_WAVES")) {
-        const int w = std::atoi(env);
-        if (w > 0) {
-            out.waves4 = std::min(out.waves4, w);
-            out.waves8 = std::min(out.waves8, w);
+    // Tuning override: fewer workgroups than the device holds (never more,
+    // since every workgroup owns a fixed share of the work).
+    if (const char* env = std::getenv("WQ_GROUPED_BLOCKS")) {
+        const int b = std::atoi(env);
+        if (b > 0) {
+            out.blocks4 = std::min(out.blocks4, b);
+            out.blocks8 = std::min(out.blocks8, b);
         }
     }
     // Tuning override: the vector small-batch kernel's target wave count.
@@ -219,8 +240,9 @@ hipError_t launch_groups(const wq_linear* lin, const Group* groups, int ngroups,
             p.entries = reinterpret_cast<const DecodeEntry*>(d_plan + gp.off_entries);
             p.classes = reinterpret_cast<const DecodeClass*>(d_plan + gp.off_classes);
             p.class_lin = reinterpret_cast<const int32_t*>(d_plan + gp.off_list);
+            p.blocks = reinterpret_cast<const DecodeBlock*>(d_plan + gp.off_blocks);
             p.nclasses = gp.nclasses;
-            e = launch_grouped_m1(p, gp.max_gpl, gp.waves, stream);
+            e = launch_grouped_m1(p, gp.max_gpl, gp.blocks, stream);
         } else {
             const BatchPlan& bp = bplans[i];
             const DecodeEntry* ents = reinterpret_cast<const DecodeEntry*>(d_plan + bp.off_entries);

@@ -335,13 +335,13 @@ def wq_fused_check(device=None, stream=None) -> None:
 
 def stream_read(buf, sink, stream=None) -> None:
     """Read the whole device tensor `buf` once (wq_stream_read); `sink` is a
-    device int32/uint32 tensor of at least 2048 elements."""
+    device int32/uint32 tensor of at least 1024 elements."""
     import torch
 
     if buf.device.type != "cuda" or not buf.is_contiguous():
         raise ValueError("buf must be a contiguous device tensor")
     nbytes = buf.numel() * buf.element_size()
-    if sink.device != buf.device or sink.dtype not in (torch.int32, torch.uint32) or sink.numel() < 2048:
-        raise ValueError("sink must be a device int32 tensor of at least 2048 elements")
+    if sink.device != buf.device or sink.dtype not in (torch.int32, torch.uint32) or sink.numel() < 1024:
+        raise ValueError("sink must be a device int32 tensor of at least 1024 elements")
     _check(lib().wq_stream_read(ctypes.c_void_p(buf.data_ptr()), nbytes, ctypes.c_void_p(sink.data_ptr()),
                                 _stream(stream, buf.device)))
