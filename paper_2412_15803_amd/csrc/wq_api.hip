@@ -263,7 +263,7 @@ wq_status decode_grouped(const char* fn, const wq_linear* lin, int64_t count, in
     std::lock_guard<std::mutex> guard(g_ws_mu);
     DecodeWorkspace* ws = nullptr;
     if ((st = get_workspace(fn, stream, ws)) != WQ_OK) return st;
-    const bool matrix = m >= wq::kMatrixCoreMinM && !wq::vector_small_batch();
+    const bool matrix = wq::use_matrix_cores(m);
     std::vector<unsigned char> bytes(
         wq::plan::plan_bytes_bound(count, std::max(ws->shape.blocks4, ws->shape.blocks8)));
     PlanBuf pb{bytes.data(), bytes.size(), 0, false};

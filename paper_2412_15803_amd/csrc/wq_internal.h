@@ -40,9 +40,12 @@ constexpr int kMaxSmallBatchM = 64;
 hipError_t launch_prefill(const uint32_t* packed, const uint16_t* scales, const uint16_t* x, uint16_t* y,
                           int64_t n, int64_t k, int64_t m, hipStream_t stream);
 
-// WQ_SMALL_BATCH_VECTOR=1 in the environment sends every small batch to the
-// vector kernel (for comparing the two paths; read at every call).
-bool vector_small_batch();
+// Whether a small batch of m rows (2 <= m <= kMaxSmallBatchM) runs on the
+// matrix cores: from kMatrixCoreMinM rows on.  Tuning overrides, read at
+// every call (for comparing the two paths): WQ_SMALL_BATCH_VECTOR=1 sends
+// every small batch to the vector kernel, WQ_MATRIX_MIN_M=n moves the
+// threshold to n.
+bool use_matrix_cores(int64_t m);
 
 // y[M][N] for 2 <= M on the matrix cores, 16 batch rows per launch.
 hipError_t launch_gemm_mfma(const uint32_t* packed, const uint16_t* scales, const uint16_t* x, uint16_t* y,
@@ -101,9 +104,12 @@ struct DecodePlan {
 
 // Small-batch decode step: independent linears in one launch of the matrix-core
 // kernel.  Entry i owns blocks [first_step, first_step + steps) of the grid,
-// each block grouped_mfma_tiles() tiles of 16 rows, waves_per_block <= 8;
+// each block grouped_mfma_tiles() tiles of 16 rows, waves_per_block <=
+// grouped_mfma_max_waves();
 // batch rows [m0, m0 + m), m <= 16.
 int grouped_mfma_tiles();
+// Most waves a block of the matrix-core kernels has (LDS per wave).
+int grouped_mfma_max_waves();
 hipError_t launch_grouped_mfma(const DecodeEntry* entries, int count, int64_t blocks, int waves_per_block,
                                int64_t m0, int m, hipStream_t stream);
 

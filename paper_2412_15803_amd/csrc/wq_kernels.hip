@@ -496,9 +496,15 @@ int mb_rows_for_work(int64_t work, int64_t ng) {
     return (int)min((int64_t)kMbRows, max((int64_t)kMbStep, (r + kMbStep - 1) / kMbStep * kMbStep));
 }
 
-bool vector_small_batch() {
-    const char* e = std::getenv("WQ_SMALL_BATCH_VECTOR");
-    return e && e[0] == '1';
+bool use_matrix_cores(int64_t m) {
+    const char* v = std::getenv("WQ_SMALL_BATCH_VECTOR");
+    if (v && v[0] == '1') return false;
+    int64_t min_m = kMatrixCoreMinM;
+    if (const char* e = std::getenv("WQ_MATRIX_MIN_M")) {
+        const long long t = std::atoll(e);
+        if (t >= 2) min_m = t;
+    }
+    return m >= min_m;
 }
 
 hipError_t launch_pack(const float* w, uint32_t* packed, uint16_t* scales, int64_t n, int64_t k,
@@ -527,7 +533,7 @@ hipError_t launch_gemv(const uint32_t* packed, const uint16_t* scales, const uin
         // Matrix cores from 8 batch rows on (measured faster than the vector
         // kernel there); below that, or when asked to, the vector kernel in
         // passes of up to 8 rows.
-        if (m >= kMatrixCoreMinM && !vector_small_batch()) return launch_gemm_mfma(packed, scales, x, y, n, k, m, stream);
+        if (use_matrix_cores(m)) return launch_gemm_mfma(packed, scales, x, y, n, k, m, stream);
         for (int64_t m0 = 0; m0 < m; m0 += 8) {
             const int mc = (int)min((int64_t)8, m - m0);
             const uint16_t* xc = x + m0 * k;

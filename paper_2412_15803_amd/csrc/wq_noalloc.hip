@@ -155,7 +155,7 @@ extern "C" wq_status wq_decode_linears_noalloc(const wq_linear* linears, int64_t
         plan::SpanList reads(g_reads, kMaxLinears), writes(g_writes, kMaxLinears);
         plan::split_groups(linears, (int)count, M, reads, writes, [&](const Group& g) { g_groups[ngroups++] = g; });
     }
-    const bool matrix = M >= kMatrixCoreMinM && !vector_small_batch();
+    const bool matrix = use_matrix_cores(M);
     const int64_t target = ds->shape.mb_waves[M <= 2 ? 0 : M <= 4 ? 1 : 2];
     PlanBuf pb{g_plan, kScratchBytes, 0, false};
     for (int i = 0; i < ngroups; ++i) {

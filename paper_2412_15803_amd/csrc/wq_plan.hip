@@ -160,8 +160,9 @@ BatchPlan plan_batch_group(const wq_linear* lin, const Group& g, PlanBuf& out) {
     }
     bp.blocks = blocks;
     // About 32 steps of the longest row per wave (measured on the 3B- and
-    // 8B-class steps: fewer, longer waves keep more blocks resident per CU).
-    bp.waves_per_block = (int)std::min<int64_t>(8, (max_steps + 31) / 32);
+    // 8B-class steps: fewer, longer waves keep more blocks resident per CU),
+    // at most 4 (each wave's scale-window slots take 16 KiB of LDS).
+    bp.waves_per_block = (int)std::min<int64_t>(grouped_mfma_max_waves(), (max_steps + 31) / 32);
     out.size = end;
     return bp;
 }

@@ -118,6 +118,15 @@ def random_scales_host(seed: int, n: int, k: int, lo: float = 1e-4, hi: float = 
     return rng.uniform(lo, hi, size=(n, k // 32)).astype(np.float16).view(np.uint16)
 
 
+def pow2_scales_host(seed: int, n: int, k: int, lo_exp: int = -10, hi_exp: int = -6) -> np.ndarray:
+    """fp16 scale bits 2^e, e drawn per (row, group) from [lo_exp, hi_exp]:
+    every scaled code is exact in fp16, so sums of small-integer x stay
+    exact while each group still has its own scale."""
+    rng = np.random.default_rng(seed)
+    e = rng.integers(lo_exp, hi_exp + 1, size=(n, k // 32))
+    return np.ldexp(np.ones_like(e, dtype=np.float64), e).astype(np.float16).view(np.uint16)
+
+
 def small_int_x_host(seed: int, m: int, k: int, lim: int = 4) -> np.ndarray:
     rng = np.random.default_rng(seed)
     return rng.integers(-lim, lim + 1, size=(m, k)).astype(np.float16)

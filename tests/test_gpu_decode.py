@@ -325,6 +325,25 @@ def test_small_batch_independent_linears_bit_exact(m):
         check_exact(lin[3], oracle.gemv(p, s, x, n, k), f"M={m} {n}x{k}")
 
 
+@pytest.mark.parametrize("m", [8, 16])
+def test_small_batch_pow2_scales_bit_exact(m):
+    """Grouped matrix-core launch with a power-of-two scale per (row, group):
+    any mix-up of which lane applies which group's scale changes the bits.
+    Even and odd group counts per row (the two scale load paths)."""
+    shapes = [(300, 1056), (520, 4096), (77, 3104), (131, 14336), (1000, 2080)]
+    announce(f"decode small batch M={m}, power-of-two scales")
+    host, lins = [], []
+    for i, (n, k) in enumerate(shapes):
+        p = wl.random_words_host(400 + i, n, k)
+        s = wl.pow2_scales_host(500 + i, n, k)
+        x = wl.small_int_x_host(600 + i, m, k, lim=3)
+        host.append((p, s, x))
+        lins.append((to_dev(p), to_dev(s), to_dev(x), nan_out(m, n)))
+    run(lins, m=m)
+    for (p, s, x), lin, (n, k) in zip(host, lins, shapes):
+        check_exact(lin[3], oracle.gemv(p, s, x, n, k), f"M={m} {n}x{k}")
+
+
 @pytest.mark.parametrize("m", [2, 3, 5])
 def test_small_batch_3b_layer_bit_exact(m):
     """The 3B layer's four linears (96-group rows walked in 32-group tiles,

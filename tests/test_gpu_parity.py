@@ -245,6 +245,19 @@ def test_gemv_integer_exact_random_shapes_m1_and_matrix_cores(n, k, m):
     _gemv_case(p, s, x, None, True, "integer-exact random shape")
 
 
+@pytest.mark.parametrize("n,k,m", [(16, 32, 8), (40, 96, 16), (257, 544, 9), (300, 1056, 16), (1000, 2080, 12),
+                                   (520, 4096, 16), (131, 14336, 8), (77, 3104, 13)], ids=lambda v: str(v))
+def test_gemv_pow2_scales_matrix_cores_bit_exact(n, k, m):
+    """A power-of-two scale per (row, group) and small-integer x keep every
+    sum exact, so any mix-up of which lane applies which group's scale
+    changes the bits.  Even and odd numbers of groups per row (the two scale
+    load paths), one to several waves per block, ragged N."""
+    p = wl.random_words_host(n * 11 + k + m, n, k)
+    s = wl.pow2_scales_host(n + 5 * k + m, n, k)
+    x = wl.small_int_x_host(2 * n + k + 3 * m, m, k, lim=3)
+    _gemv_case(p, s, x, None, True, "power-of-two scales")
+
+
 @pytest.mark.parametrize("n,k,m", _random_small_batch_shapes(24, 2024), ids=lambda v: str(v))
 def test_gemv_integer_exact_small_batch_random_shapes(n, k, m):
     p = wl.random_words_host(n * 7 + k * 3 + m, n, k)
