@@ -99,7 +99,7 @@ wq_status wq_pack(const float* w, uint32_t* packed_w, uint16_t* scales,
  *   N, K, M   1 <= N <= WQ_MAX_N, 32 <= K <= WQ_MAX_K, 1 <= M <= WQ_MAX_M.
  *   group     must be 32.
  * Accumulation is fp32; each output is rounded once to fp16 (round to
- * nearest even).  For M < 8 every product is exact.  For M >= 8 (matrix
+ * nearest even).  For M <= 2 every product is exact.  For M >= 3 (matrix
  * cores) each scaled weight (q - 8) * s is first rounded to fp16 (relative
  * error <= 2^-11); this needs |(q - 8) * s| <= 65504, i.e. scales below 8188,
  * and larger scales give infinities on that path.  Per element the result is

@@ -27,9 +27,11 @@ hipError_t launch_gemv(const uint32_t* packed, const uint16_t* scales,
                        const uint16_t* x, uint16_t* y,
                        int64_t n, int64_t k, int64_t m, hipStream_t stream);
 
-// Smallest batch that uses the matrix cores; smaller batches run on the
-// vector ALUs.
-constexpr int kMatrixCoreMinM = 8;
+// Smallest batch that uses the matrix cores; M = 2 runs on the vector ALUs.
+// Measured on the 3B- and 8B-class decode steps: the matrix cores are faster
+// from M = 3 on (3B step at M = 4: 435 against 475 us; 8B step at M = 7: 930
+// against 1624 us), the vector kernel at M = 2 (395 against 479 us).
+constexpr int kMatrixCoreMinM = 3;
 
 // Largest batch of the small-batch kernels; larger ones (prompts) run the
 // tiled prefill GEMM.
@@ -113,7 +115,8 @@ int grouped_mfma_max_waves();
 hipError_t launch_grouped_mfma(const DecodeEntry* entries, int count, int64_t blocks, int waves_per_block,
                                int64_t m0, int m, hipStream_t stream);
 
-// Small-batch decode step below kMatrixCoreMinM rows: independent linears in
+// Small-batch decode step below kMatrixCoreMinM rows (or any small batch when
+// forced): independent linears in
 // one launch of the vector kernel.  Entry i owns waves [first_step,
 // first_step + steps) of the grid, `pad` rows each (a multiple of 8, at most
 // 256); batch rows [m0, m0 + m), m <= 8.

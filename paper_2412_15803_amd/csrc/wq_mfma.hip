@@ -1,6 +1,6 @@
 // Small-batch 4-bit GEMM on the matrix cores: y[M][N] = x[M][K] dequant(W)^T
-// for up to 16 batch rows per launch, used from M = 8 on (smaller batches
-// run on the vector kernel).  Batching several sequences is this library's
+// for up to 16 batch rows per launch, used from M = 3 on (M = 2 runs on the
+// vector kernel).  Batching several sequences is this library's
 // extension of the paper's batch-1 decoding; the tiling follows the
 // operator-level GEMM tiling the paper's compiler applies (Sec. 2.3).
 //
@@ -113,15 +113,25 @@ __device__ __forceinline__ void issue_scale_window(const __amdgpu_buffer_rsrc_t&
 }
 
 // The lane's scale bits from LDS (byte address `addr`).  An LDS read the
-// compiler sees after a direct-to-LDS load would get a wait for every load
-// in flight (it cannot tell the slots apart), so the read is written out
-// here and ordered by hand: `after` is a value computed from the item's
-// codes, whose load was issued after the window's scale load, so the codes
-// having arrived means (loads retire in order) the scales have too.  The
-// wait covers the read itself.
-__device__ __forceinline__ uint32_t lds_scale(uint32_t addr, uint32_t after) {
+// compiler sees after a direct-to-LDS load gets a wait for every load in
+// flight (it cannot tell the window slots apart), so the read is written
+// out here and ordered by data dependences instead:
+//   * `w` (a code register of the item) passes through the read: the read
+//     is issued once the item's codes have arrived, and their load was
+//     issued after the window's scale load (loads retire in order);
+//   * the code register that comes out is what the item's permutes take,
+//     so they are issued after the read;
+//   * lds_scale_ready() hands the scale on only together with a permuted
+//     word: the compiler waits for that permute before using it, and LDS
+//     operations of a wave complete in order, so the read has completed.
+__device__ __forceinline__ uint32_t lds_scale_read(uint32_t addr, uint32_t& w) {
     uint32_t v;
-    asm volatile("ds_read_u16 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(addr), "v"(after) : "memory");
+    asm volatile("ds_read_u16 %0, %2" : "=&v"(v), "+v"(w) : "v"(addr) : "memory");
+    return v;
+}
+
+__device__ __forceinline__ uint32_t lds_scale_ready(uint32_t v, uint32_t permuted) {
+    asm volatile("" : "+v"(v) : "v"(permuted));
     return v;
 }
 
@@ -134,11 +144,12 @@ __device__ __forceinline__ uint32_t lds_scale(uint32_t addr, uint32_t after) {
 template <int SM>
 __device__ __forceinline__ void compute_item(const MItem& b, const half8 (&xa)[4], float4v& acc, uint32_t keep,
                                              int baddr, uint32_t saddr) {
-    const uint32_t wd[4] = {to_mfma(b.w.x, baddr), to_mfma(b.w.y, baddr), to_mfma(b.w.z, baddr),
+    uint32_t w0 = b.w.x, sv = 0;
+    if constexpr (SM == kScaleLds) sv = lds_scale_read(saddr, w0);
+    const uint32_t wd[4] = {to_mfma(w0, baddr), to_mfma(b.w.y, baddr), to_mfma(b.w.z, baddr),
                             to_mfma(b.w.w, baddr)};
-    uint32_t sv;
     if constexpr (SM == kScaleItem) sv = to_mfma(b.s, baddr) & 0xFFFFu;
-    else sv = lds_scale(saddr, wd[0]);
+    else sv = lds_scale_ready(sv, wd[0]);
     // (q - 8) * s rounded once to fp16: the weights in the scale of operand
     // B, so the multiplies accumulate across groups.
     const half2v sc = as_h2((sv | (sv << 16)) & keep);
@@ -214,7 +225,10 @@ __host__ __device__ constexpr int block_lds_bytes(int t, int sm, int waves) {
 // and are never used.  The waves' partial tiles are summed through LDS in a
 // fixed order and one wave per tile rounds and stores it.  `lds` is the
 // block's dynamic LDS, wave_lds_bytes(T, SM) per wave.
-constexpr int kDepth = 8;
+#ifndef WQ_MFMA_DEPTH
+#define WQ_MFMA_DEPTH 8
+#endif
+constexpr int kDepth = WQ_MFMA_DEPTH;
 
 template <int T, int SM>
 __device__ __forceinline__ void mfma_block(const void* packed, const uint16_t* scales, const uint16_t* x,

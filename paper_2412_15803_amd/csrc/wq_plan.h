@@ -169,7 +169,7 @@ struct BatchPlan {
 // wide grouped kernels.
 GroupPlan plan_group(const wq_linear* lin, const Group& g, int capacity4, int capacity8, PlanBuf& out);
 
-// Append the matrix-core (M >= 8) plan of a group.
+// Append the matrix-core (M >= 3) plan of a group.
 BatchPlan plan_batch_group(const wq_linear* lin, const Group& g, PlanBuf& out);
 
 // Append the vector small-batch (M < 8) plan of a group, `target` waves.

@@ -135,6 +135,11 @@ GroupPlan plan_group(const wq_linear* lin, const Group& g, int capacity4, int ca
     return gp;
 }
 
+#ifndef WQ_MFMA_WAVE_STEPS
+#define WQ_MFMA_WAVE_STEPS 32
+#endif
+constexpr int64_t kMfmaWaveSteps = WQ_MFMA_WAVE_STEPS;
+
 BatchPlan plan_batch_group(const wq_linear* lin, const Group& g, PlanBuf& out) {
     const int count = g.end - g.begin;
     const int rows_per_block = 16 * grouped_mfma_tiles();
@@ -162,7 +167,7 @@ BatchPlan plan_batch_group(const wq_linear* lin, const Group& g, PlanBuf& out) {
     // About 32 steps of the longest row per wave (measured on the 3B- and
     // 8B-class steps: fewer, longer waves keep more blocks resident per CU),
     // at most 4 (each wave's scale-window slots take 16 KiB of LDS).
-    bp.waves_per_block = (int)std::min<int64_t>(grouped_mfma_max_waves(), (max_steps + 31) / 32);
+    bp.waves_per_block = (int)std::min<int64_t>(grouped_mfma_max_waves(), (max_steps + kMfmaWaveSteps - 1) / kMfmaWaveSteps);
     out.size = end;
     return bp;
 }

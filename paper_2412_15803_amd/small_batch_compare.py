@@ -7,7 +7,7 @@
 
 For each shape and batch size M, the same wq_gemv calls run once through the
 vector-ALU kernel (WQ_SMALL_BATCH_VECTOR=1, read by the library at every
-call) and once through the default path (matrix cores from M = 8 on).
+call) and once through the default path (matrix cores from M = 3 on).
 Calls rotate over copies of random codes and scales totalling >= 1 GiB, so
 every call streams its weights from HBM.
 """
@@ -94,7 +94,7 @@ def summarise(trace_dir, out):
              "```", "",
              f"Per case: {CALLS} timed wq_gemv calls after 3 warm-up calls, rotating over >= 1 GiB of weight copies. "
              "Kernel time per call = sum of its launches (the vector path runs 8 batch rows per launch). "
-             "The default path is the vector kernel below M = 8 and the matrix-core kernel from M = 8 on.", "",
+             "The default path is the vector kernel at M = 2 and the matrix-core kernel from M = 3 on.", "",
              "| Shape N x K | M | Path | Kernel | Launches per call | Kernel us per call (avg) | GB/s |",
              "|---|---|---|---|---|---|---|"]
     i = 0

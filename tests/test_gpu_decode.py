@@ -325,7 +325,7 @@ def test_small_batch_independent_linears_bit_exact(m):
         check_exact(lin[3], oracle.gemv(p, s, x, n, k), f"M={m} {n}x{k}")
 
 
-@pytest.mark.parametrize("m", [8, 16])
+@pytest.mark.parametrize("m", [3, 8, 16])
 def test_small_batch_pow2_scales_bit_exact(m):
     """Grouped matrix-core launch with a power-of-two scale per (row, group):
     any mix-up of which lane applies which group's scale changes the bits.
@@ -406,9 +406,9 @@ def test_small_batch_decode_random_data_tolerance(m):
         assert ok.all(), f"M={m} {n}x{k}: {(~ok).sum()} outside tolerance"
 
 
-@pytest.mark.parametrize("m", [8, 16])
+@pytest.mark.parametrize("m", [3, 6, 8, 16])
 def test_small_batch_both_paths_bit_exact(m, monkeypatch):
-    """From M = 8 on the matrix cores are the default; the vector kernel
+    """From M = 3 on the matrix cores are the default; the vector kernel
     (forced through WQ_SMALL_BATCH_VECTOR, read by the library at every call)
     must give the same exact results, single GEMV and decode step alike."""
     from paper_2412_15803_amd import wq

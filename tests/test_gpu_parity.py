@@ -180,15 +180,27 @@ def test_gemv_integer_exact_small_batch(n, k, m):
     _gemv_case(p, s, x, sample_rows(n, 256, 11), True, "integer-exact")
 
 
+def _use_path(monkeypatch, path):
+    """'vector' forces the vector small-batch kernel (the library reads
+    WQ_SMALL_BATCH_VECTOR at every call); 'default' takes the library's
+    choice (the vector kernel at M = 2, the matrix cores from M = 3)."""
+    if path == "vector":
+        monkeypatch.setenv("WQ_SMALL_BATCH_VECTOR", "1")
+    else:
+        monkeypatch.delenv("WQ_SMALL_BATCH_VECTOR", raising=False)
+
+
 # Group counts that the vector small-batch kernel walks in 32-group tiles
 # with two row sets per wave (96 and 160 groups: an odd multiple of 32; 1, 2,
 # 31 and 32 groups: below one 64-group tile), and the 3B layer's widths.
 SHAPES_32_GROUP_TILES = SHAPES_3B + [(1, 32), (3, 64), (33, 992), (8, 1024), (1000, 5120)]
 
 
+@pytest.mark.parametrize("path", ["vector", "default"])
 @pytest.mark.parametrize("n,k", SHAPES_32_GROUP_TILES, ids=lambda v: str(v))
 @pytest.mark.parametrize("m", [2, 3, 4, 7])
-def test_gemv_integer_exact_small_batch_32_group_tiles(n, k, m):
+def test_gemv_integer_exact_small_batch_32_group_tiles(n, k, m, path, monkeypatch):
+    _use_path(monkeypatch, path)
     p = wl.random_words_host(5 * n + k + m, n, k)
     s = wl.constant_scales_host(n, k, 0x2400)
     x = wl.small_int_x_host(n + 7 * k + m, m, k)
@@ -202,9 +214,11 @@ def test_gemv_integer_exact_small_batch_32_group_tiles(n, k, m):
 SHAPES_K_SPLIT = [(37, 8192), (1001, 5120), (5, 16384), (3, 4096)]
 
 
+@pytest.mark.parametrize("path", ["vector", "default"])
 @pytest.mark.parametrize("n,k", SHAPES_K_SPLIT, ids=lambda v: str(v))
 @pytest.mark.parametrize("m", [2, 3, 5, 7])
-def test_gemv_integer_exact_small_batch_k_split(n, k, m):
+def test_gemv_integer_exact_small_batch_k_split(n, k, m, path, monkeypatch):
+    _use_path(monkeypatch, path)
     p = wl.random_words_host(11 * n + k + m, n, k)
     s = wl.constant_scales_host(n, k, 0x2400)
     x = wl.small_int_x_host(3 * n + 5 * k + m, m, k)
@@ -246,7 +260,8 @@ def test_gemv_integer_exact_random_shapes_m1_and_matrix_cores(n, k, m):
 
 
 @pytest.mark.parametrize("n,k,m", [(16, 32, 8), (40, 96, 16), (257, 544, 9), (300, 1056, 16), (1000, 2080, 12),
-                                   (520, 4096, 16), (131, 14336, 8), (77, 3104, 13)], ids=lambda v: str(v))
+                                   (520, 4096, 16), (131, 14336, 8), (77, 3104, 13), (64, 256, 3), (999, 4096, 5),
+                                   (200, 8192, 7)], ids=lambda v: str(v))
 def test_gemv_pow2_scales_matrix_cores_bit_exact(n, k, m):
     """A power-of-two scale per (row, group) and small-integer x keep every
     sum exact, so any mix-up of which lane applies which group's scale
@@ -258,8 +273,10 @@ def test_gemv_pow2_scales_matrix_cores_bit_exact(n, k, m):
     _gemv_case(p, s, x, None, True, "power-of-two scales")
 
 
+@pytest.mark.parametrize("path", ["vector", "default"])
 @pytest.mark.parametrize("n,k,m", _random_small_batch_shapes(24, 2024), ids=lambda v: str(v))
-def test_gemv_integer_exact_small_batch_random_shapes(n, k, m):
+def test_gemv_integer_exact_small_batch_random_shapes(n, k, m, path, monkeypatch):
+    _use_path(monkeypatch, path)
     p = wl.random_words_host(n * 7 + k * 3 + m, n, k)
     s = wl.constant_scales_host(n, k, 0x2400)
     x = wl.small_int_x_host(n + k + 17 * m, m, k)
