@@ -236,10 +236,24 @@ __device__ __forceinline__ void run_block(const DecodePlan& p, const DecodeClass
     // wave's first chunk is at most a few steps further.
     it.idx = b.pos;
     load_linear(it, p, c);
+    // x of the linear holding the wave's first step is loaded before any
+    // weight load.  Loaded later (when that step is computed, as for the
+    // linears the wave enters afterwards), it would be the youngest load in
+    // flight and the first computation would wait for the whole pipeline:
+    // in a one-layer call that is most of a wave's work, and its compute
+    // then followed all of its data instead of overlapping it.
+    while (it.pos >= it.lin_end) {
+        ++it.idx;
+        load_linear(it, p, c);
+    }
     XSlot<MAXG> xs;
-    xs.lin = -1;
-    xs.y = nullptr;
-    xs.ybase = xs.yend = 0;
+    {
+        const DecodeEntry& e = p.entries[it.cur.lin];
+        load_x_lane<LPR, GPL, MAXG>(e.x, it.cur.ng, lane, xs.xr);
+        xs.lin = it.cur.lin;
+        xs.y = e.y;
+        xs.ybase = xs.yend = (it.pos - it.first_step) * R;
+    }
     StepBuf buf[NB];
     Step st[NB];
 #pragma unroll
