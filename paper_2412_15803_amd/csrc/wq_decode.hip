@@ -34,7 +34,13 @@ using namespace dev;
 
 // Waves of one workgroup: what a CU holds of the narrow (MAXG <= 4, three
 // waves per SIMD) and the wide variant (two per SIMD).
-__host__ __device__ constexpr int cu_waves(int maxg) { return maxg <= 4 ? 12 : 8; }
+#ifndef WQ_GROUPED_WAVES4
+#define WQ_GROUPED_WAVES4 12
+#endif
+#ifndef WQ_GROUPED_WAVES8
+#define WQ_GROUPED_WAVES8 8
+#endif
+__host__ __device__ constexpr int cu_waves(int maxg) { return maxg <= 4 ? WQ_GROUPED_WAVES4 : WQ_GROUPED_WAVES8; }
 
 // What computing a step needs (the linear, its rows, its groups per row);
 // issuing it also needs the linear's pointers, which the step iterator holds

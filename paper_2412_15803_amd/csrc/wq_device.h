@@ -152,15 +152,17 @@ __device__ __forceinline__ float segment_sum(float v) {
 #define WQ_STEP_LOADS 6
 #endif
 
-__host__ __device__ constexpr int step_rows_per_slot(int gpl) {
-    return gpl >= WQ_STEP_LOADS ? 1 : WQ_STEP_LOADS / gpl;
+__host__ __device__ constexpr int step_rows_per_slot(int gpl, int loads = WQ_STEP_LOADS) {
+    return gpl >= loads ? 1 : loads / gpl;
 }
 
-template <int LPR, int GPL>
+// A kernel may take steps of fewer loads (LOADS, at most 8) than the decode
+// step's.
+template <int LPR, int GPL, int LOADS = WQ_STEP_LOADS>
 struct StepShape {
     static constexpr int SLOTS = kWave / LPR;
-    static constexpr int U = step_rows_per_slot(GPL);  // rows per slot
-    static constexpr int ROWS = U * SLOTS;             // rows per step
+    static constexpr int U = step_rows_per_slot(GPL, LOADS);  // rows per slot
+    static constexpr int ROWS = U * SLOTS;                    // rows per step
 };
 
 // One step's loads: per row and group, the 16-byte group of codes and its
@@ -245,9 +247,9 @@ __device__ __forceinline__ LinearRsrc make_rsrc(const void* packed, const uint16
 // Issue the loads of rows [row0, row0 + ROWS) of a linear with ng groups per
 // row.  Lanes whose group index runs past the row read the next row's codes
 // (or zeros at the end); their x is zero, so those codes add nothing.
-template <int LPR, int GPL, int CPOL = kCpolDefault>
+template <int LPR, int GPL, int CPOL = kCpolDefault, int LOADS = WQ_STEP_LOADS>
 __device__ __forceinline__ void issue_step(StepBuf& b, const LinearRsrc& r, int64_t row0, int ng, int lane) {
-    using S = StepShape<LPR, GPL>;
+    using S = StepShape<LPR, GPL, LOADS>;
     const int slot = lane / LPR;
     const int sub = lane & (LPR - 1);
     // This lane's group index relative to the step's first group.
@@ -280,10 +282,10 @@ using wq::fits_rsrc;
 // step's loads would then also wait for those stores.)  Lanes past the
 // row's groups hold zero x, so their (clamped, finite) codes contribute
 // nothing.
-template <int LPR, int GPL, int MAXG>
+template <int LPR, int GPL, int MAXG, int LOADS = WQ_STEP_LOADS>
 __device__ __forceinline__ void compute_step(const StepBuf& b, const half2v (&xr)[MAXG][16], int nrows,
                                              uint16_t* ylds, int yrel, int lane) {
-    using S = StepShape<LPR, GPL>;
+    using S = StepShape<LPR, GPL, LOADS>;
     const int slot = lane / LPR;
     const int sub = lane & (LPR - 1);
 #pragma unroll

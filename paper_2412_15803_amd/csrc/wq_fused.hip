@@ -41,7 +41,24 @@ using namespace dev;
 
 constexpr int kBlock = 256;
 constexpr int kWavesPerBlock = kBlock / kWave;
-constexpr int kTargetWaves = 256 * 8;
+// Launch shape and loads, as for the single-linear GEMV: about 1024 waves,
+// steps of four 16-byte loads per lane and non-temporal weight loads.
+// Measured on the dependent 3B step (113 launches per token): 899 us per
+// token with 2048 waves, six-load steps and the default policy; 857 with the
+// loads past a wave's last step no longer reading the next wave's rows; 767
+// with 1024 waves; 723 with four-load steps; 675-683 with non-temporal
+// loads (512 waves: 870, 768: 740; two- or three-load steps: the same).
+#ifndef WQ_FUSED_WAVES
+#define WQ_FUSED_WAVES (256 * 4)
+#endif
+#ifndef WQ_FUSED_STEP_LOADS
+#define WQ_FUSED_STEP_LOADS 4
+#endif
+#ifndef WQ_FUSED_CPOL
+#define WQ_FUSED_CPOL kCpolNonTemporal
+#endif
+constexpr int kTargetWaves = WQ_FUSED_WAVES;
+constexpr int kFLoads = WQ_FUSED_STEP_LOADS;
 constexpr int kMaxK = (int)WQ_FUSED_MAX_K;
 constexpr int kArgThreads = 1024;
 
@@ -195,10 +212,10 @@ __device__ __forceinline__ void load_x_lane_lds(const uint16_t* s_x, int ng, int
 }
 
 // compute_step with the row sums staged as fp32 (the residual is added later).
-template <int LPR, int GPL>
+template <int LPR, int GPL, int LOADS = WQ_STEP_LOADS>
 __device__ __forceinline__ void compute_step_f32(const StepBuf& b, const half2v (&xr)[GPL][16], int nrows,
                                                  float* ylds, int yrel, int lane) {
-    using S = StepShape<LPR, GPL>;
+    using S = StepShape<LPR, GPL, LOADS>;
     const int slot = lane / LPR;
     const int sub = lane & (LPR - 1);
 #pragma unroll
@@ -230,7 +247,7 @@ __device__ __forceinline__ void flush_y_residual(uint16_t* y, const uint16_t* re
 
 template <int LPR, int GPL>
 __global__ __launch_bounds__(kBlock) void fused_m1_kernel(const Args a) {
-    constexpr int R = StepShape<LPR, GPL>::ROWS;
+    constexpr int R = StepShape<LPR, GPL, kFLoads>::ROWS;
     extern __shared__ __align__(16) uint16_t s_x[];  // x_eff, K entries (prologues only)
     __shared__ __align__(16) float s_y[kWavesPerBlock][kYRows];
     __shared__ float s_red[kWavesPerBlock];
@@ -248,8 +265,11 @@ __global__ __launch_bounds__(kBlock) void fused_m1_kernel(const Args a) {
         // while x is rearranged and the prologue computed, and waiting for x
         // never waits for them (the load counter retires in issue order).
         // Waves past the matrix take part in the prologue's barriers; their
-        // loads read zeros.
+        // loads read zeros.  Loads of steps past the wave's last one start
+        // at row n, past the end of the codes and scales: they read zeros
+        // without touching memory instead of another wave's rows.
         const int64_t steps = rb < a.n ? (re - rb + R - 1) / R : 0;
+        const auto row_of = [&](int64_t st) { return st < steps ? rb + st * R : a.n; };
         const LinearRsrc rs = make_rsrc(a.packed, a.scales, (uint32_t)(a.n * a.ng * 2));
         if (a.prologue != WQ_PROLOGUE_NONE) {
             // 8-element chunks of x per thread for the longest row of this
@@ -258,28 +278,28 @@ __global__ __launch_bounds__(kBlock) void fused_m1_kernel(const Args a) {
             // weight loads issued beside them.
             constexpr int CPT = (LPR * GPL * kGroup / 8 + kBlock - 1) / kBlock;
             stage_prologue<CPT>(a, s_x, s_red, [&] {
-                issue_step<LPR, GPL>(b0, rs, rb, a.ng, lane);
-                issue_step<LPR, GPL>(b1, rs, rb + R, a.ng, lane);
+                issue_step<LPR, GPL, WQ_FUSED_CPOL, kFLoads>(b0, rs, row_of(0), a.ng, lane);
+                issue_step<LPR, GPL, WQ_FUSED_CPOL, kFLoads>(b1, rs, row_of(1), a.ng, lane);
             });
             load_x_lane_lds<LPR, GPL>(s_x, a.ng, lane, xr);
         } else {
             u32x4 raw[GPL][4];
             x_lane_raw<LPR, GPL>(a.x, a.ng, lane, raw);
-            issue_step<LPR, GPL>(b0, rs, rb, a.ng, lane);
-            issue_step<LPR, GPL>(b1, rs, rb + R, a.ng, lane);
+            issue_step<LPR, GPL, WQ_FUSED_CPOL, kFLoads>(b0, rs, row_of(0), a.ng, lane);
+            issue_step<LPR, GPL, WQ_FUSED_CPOL, kFLoads>(b1, rs, row_of(1), a.ng, lane);
             x_lane_pair<LPR, GPL>(raw, a.ng, lane, xr);
         }
         if (rb >= a.n) return;
-        // As in gemv_m1_kernel: unconditional issues (past the matrix the
-        // loads read zeros), so the wait counts stay exact.
+        // As in gemv_m1_kernel: unconditional issues, so the wait counts
+        // stay exact.
         for (int64_t s = 0; s < steps; s += 2) {
             const int64_t ra = rb + s * R;
-            compute_step_f32<LPR, GPL>(b0, xr, (int)min((int64_t)R, re - ra), ylds, (int)(s * R), lane);
-            issue_step<LPR, GPL>(b0, rs, ra + 2 * R, a.ng, lane);
+            compute_step_f32<LPR, GPL, kFLoads>(b0, xr, (int)min((int64_t)R, re - ra), ylds, (int)(s * R), lane);
+            issue_step<LPR, GPL, WQ_FUSED_CPOL, kFLoads>(b0, rs, row_of(s + 2), a.ng, lane);
             const int64_t rbb = ra + R;
             if (s + 1 < steps)
-                compute_step_f32<LPR, GPL>(b1, xr, (int)min((int64_t)R, re - rbb), ylds, (int)((s + 1) * R), lane);
-            issue_step<LPR, GPL>(b1, rs, rbb + 2 * R, a.ng, lane);
+                compute_step_f32<LPR, GPL, kFLoads>(b1, xr, (int)min((int64_t)R, re - rbb), ylds, (int)((s + 1) * R), lane);
+            issue_step<LPR, GPL, WQ_FUSED_CPOL, kFLoads>(b1, rs, row_of(s + 3), a.ng, lane);
         }
     } else {
         // Rows of more than 256 groups: x first, then the weights (their x
@@ -294,15 +314,16 @@ __global__ __launch_bounds__(kBlock) void fused_m1_kernel(const Args a) {
         }
         if (rb >= a.n) return;
         const int64_t steps = (re - rb + R - 1) / R;
+        const auto row_of = [&](int64_t st) { return st < steps ? rb + st * R : a.n; };
         const LinearRsrc rs = make_rsrc(a.packed, a.scales, (uint32_t)(a.n * a.ng * 2));
         for (int64_t s = -2; s < steps; s += 2) {
             const int64_t ra = rb + s * R;
-            if (s >= 0) compute_step_f32<LPR, GPL>(b0, xr, (int)min((int64_t)R, re - ra), ylds, (int)(s * R), lane);
-            issue_step<LPR, GPL>(b0, rs, ra + 2 * R, a.ng, lane);
+            if (s >= 0) compute_step_f32<LPR, GPL, kFLoads>(b0, xr, (int)min((int64_t)R, re - ra), ylds, (int)(s * R), lane);
+            issue_step<LPR, GPL, WQ_FUSED_CPOL, kFLoads>(b0, rs, row_of(s + 2), a.ng, lane);
             const int64_t rbb = ra + R;
             if (s + 1 >= 0 && s + 1 < steps)
-                compute_step_f32<LPR, GPL>(b1, xr, (int)min((int64_t)R, re - rbb), ylds, (int)((s + 1) * R), lane);
-            issue_step<LPR, GPL>(b1, rs, rbb + 2 * R, a.ng, lane);
+                compute_step_f32<LPR, GPL, kFLoads>(b1, xr, (int)min((int64_t)R, re - rbb), ylds, (int)((s + 1) * R), lane);
+            issue_step<LPR, GPL, WQ_FUSED_CPOL, kFLoads>(b1, rs, row_of(s + 3), a.ng, lane);
         }
     }
     flush_y_residual(a.y, a.residual, rb, ylds, (int)(re - rb), lane);
@@ -909,7 +930,7 @@ __global__ __launch_bounds__(256) void chain_epilogue(const ChainCopy* __restric
 
 template <int LPR, int GPL>
 hipError_t launch_fused(const wq_fused_linear& l, hipStream_t stream) {
-    constexpr int R = StepShape<LPR, GPL>::ROWS;
+    constexpr int R = StepShape<LPR, GPL, kFLoads>::ROWS;
     const int64_t ng = l.K / kGroup;
     const int64_t steps = (l.N + R - 1) / R;
     const int64_t steps_per_wave = std::min((steps + kTargetWaves - 1) / kTargetWaves, (int64_t)(kYRows / R));

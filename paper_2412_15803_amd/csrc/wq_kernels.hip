@@ -65,16 +65,42 @@ __global__ __launch_bounds__(kBlock) void pack_kernel(const float* __restrict__ 
 // ------------------------------------------------------------ batch-1 GEMV
 //
 // Each wave owns a contiguous block of at most kYRows rows and walks it in
-// steps through two register buffers: compute buffer A, refill A with the
-// step two ahead, compute B, refill B.  Whenever the wave waits for a buffer,
-// the other buffer's loads are still in flight.  Outputs are staged in LDS
-// and written once, after the last step.
+// steps through NB register buffers: compute buffer i, refill it with the
+// step NB ahead, move to buffer i + 1.  Whenever the wave waits for a
+// buffer, the other NB - 1 buffers' loads are in flight.  Outputs are staged
+// in LDS and written once, after the last step.
+//
+// Launch shape and pipeline, as measured on the single linears of the 3B
+// and 8B layers (cold weights): about 1024 waves (four per CU, in workgroups
+// of four), steps of four 16-byte loads per lane (the decode step's kernel
+// takes six), two buffers and the default cache policy.  Every change that
+// put more loads in flight at once made these launches slower; 8B gate_up
+// 28672x4096 took 15.1-15.3 us so, against 16.5 with six-load steps, 17.4-19.6
+// with three to six buffers, and 18.2 (2048 waves) and 21.5 us (4096 waves)
+// with six-load steps and two buffers.
+#ifndef WQ_M1_STEP_LOADS
+#define WQ_M1_STEP_LOADS 4
+#endif
+#ifndef WQ_M1_DEPTH
+#define WQ_M1_DEPTH 2
+#endif
+#ifndef WQ_M1_CPOL
+#define WQ_M1_CPOL kCpolNonTemporal
+#endif
+#ifndef WQ_M1_WAVES
+#define WQ_M1_WAVES (256 * 4)
+#endif
+constexpr int kM1Loads = WQ_M1_STEP_LOADS;
+constexpr int kM1Waves = WQ_M1_WAVES;
+static_assert(kM1Loads >= 1 && kM1Loads <= 8, "a step's loads fit StepBuf");
+
 template <int LPR, int GPL>
 __global__ __launch_bounds__(kBlock) void gemv_m1_kernel(const u32x4* packed, const uint16_t* scales,
                                                          const uint16_t* __restrict__ x,
                                                          uint16_t* __restrict__ y, int64_t n, int ng,
                                                          int64_t rows_per_wave) {
-    constexpr int R = StepShape<LPR, GPL>::ROWS;
+    constexpr int R = StepShape<LPR, GPL, kM1Loads>::ROWS;
+    constexpr int NB = WQ_M1_DEPTH;
     const int lane = threadIdx.x & (kWave - 1);
     // Wave-uniform (the compiler cannot see that threadIdx.x / 64 is), so
     // the row bookkeeping stays in scalar registers and branches uniform.
@@ -88,23 +114,33 @@ __global__ __launch_bounds__(kBlock) void gemv_m1_kernel(const u32x4* packed, co
     __shared__ __align__(16) uint16_t s_y[kWavesPerBlock][kYRows];
     uint16_t* ylds = s_y[threadIdx.x / kWave];
 
+    // x first: its loads are then the oldest in flight, and waiting for
+    // them never waits for a weight load.
     half2v xr[GPL][16];
     load_x_lane<LPR, GPL, GPL>(x, ng, lane, xr);
 
-    // The loop starts two steps early so that the first pass only issues and
-    // every load comes from the same two issue sites (one register
-    // assignment, no prologue copies that would force a full wait).  Every
-    // issue is unconditional (past the matrix the loads read zeros), so the
-    // wait counts stay exact.
-    StepBuf a, b;
-    for (int64_t s = -2; s < steps; s += 2) {
-        const int64_t ra = rb + s * R;
-        if (s >= 0) compute_step<LPR, GPL, GPL>(a, xr, (int)min((int64_t)R, re - ra), ylds, (int)(s * R), lane);
-        issue_step<LPR, GPL>(a, rs, ra + 2 * R, ng, lane);
-        const int64_t rbb = ra + R;
-        if (s + 1 >= 0 && s + 1 < steps)
-            compute_step<LPR, GPL, GPL>(b, xr, (int)min((int64_t)R, re - rbb), ylds, (int)((s + 1) * R), lane);
-        issue_step<LPR, GPL>(b, rs, rbb + 2 * R, ng, lane);
+    // Every pass issues into every buffer, also past the wave's last step:
+    // those loads start at row n, past the end of the codes and scales, and
+    // read zeros without touching memory (for codes within a step of 4 GiB
+    // the 32-bit offset can wrap to an in-range load, whose data is never
+    // used).  Every path through the loop thus issues the same loads, so the
+    // compiler's wait counts stay exact.
+    StepBuf buf[NB];
+#pragma unroll
+    for (int i = 0; i < NB; ++i)
+        issue_step<LPR, GPL, WQ_M1_CPOL, kM1Loads>(buf[i], rs, i < steps ? rb + i * R : n, ng, lane);
+    for (int64_t s = 0; s < steps; s += NB) {
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+            const int64_t si = s + i;
+            if (si < steps) {
+                const int64_t ri = rb + si * R;
+                compute_step<LPR, GPL, GPL, kM1Loads>(buf[i], xr, (int)min((int64_t)R, re - ri), ylds, (int)(si * R),
+                                                      lane);
+            }
+            issue_step<LPR, GPL, WQ_M1_CPOL, kM1Loads>(buf[i], rs, si + NB < steps ? rb + (si + NB) * R : n, ng,
+                                                       lane);
+        }
     }
     flush_y(y, rb, ylds, (int)(re - rb), lane);
 }
@@ -443,11 +479,11 @@ __global__ __launch_bounds__(kBlock) void gemv_generic_kernel(const u32x4* packe
 template <int LPR, int GPL>
 hipError_t launch_m1(const uint32_t* packed, const uint16_t* scales, const uint16_t* x, uint16_t* y,
                      int64_t n, int64_t ng, hipStream_t stream) {
-    constexpr int R = StepShape<LPR, GPL>::ROWS;
+    constexpr int R = StepShape<LPR, GPL, kM1Loads>::ROWS;
     const int64_t steps = (n + R - 1) / R;
     // At most kYRows rows per wave (its LDS staging of y); more waves than
     // the target when the matrix is taller than that allows.
-    const int64_t steps_per_wave = min((steps + kTargetWaves - 1) / kTargetWaves, (int64_t)(kYRows / R));
+    const int64_t steps_per_wave = min((steps + kM1Waves - 1) / kM1Waves, (int64_t)(kYRows / R));
     const int64_t rows_per_wave = steps_per_wave * R;
     const int64_t waves = (n + rows_per_wave - 1) / rows_per_wave;
     const int64_t blocks = (waves + kWavesPerBlock - 1) / kWavesPerBlock;
