@@ -106,7 +106,7 @@ wq_status wq_fused_linears(const wq_fused_linear* linears, int64_t count, int32_
  * only by the copy kernel at the end.  Results are bit-identical to the
  * per-linear path.  (It is not the default: on MI355X a boundary inside it
  * costs about 5 us, two agent-scope memory round trips, against about
- * 3.5 us for a kernel boundary of the per-linear path, so a whole 3B-class
+ * 3 us for a kernel boundary of the per-linear path, so a whole 3B-class
  * token takes longer this way.)
  *
  * The persistent path's library memory is part of the resident plan of the
