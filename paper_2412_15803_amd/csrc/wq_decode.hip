@@ -253,19 +253,27 @@ __device__ __forceinline__ void run_block(const DecodePlan& p, const DecodeClass
         load_linear(it, p, c);
     }
     XSlot<MAXG> xs;
+    u32x4 xraw[MAXG][4];
+    const int xng = it.cur.ng;
     {
         const DecodeEntry& e = p.entries[it.cur.lin];
-        load_x_lane<LPR, GPL, MAXG>(e.x, it.cur.ng, lane, xs.xr);
+        load_x_raw<LPR, GPL, MAXG>(e.x, xng, lane, xraw);
+        load_order_fence();
         xs.lin = it.cur.lin;
         xs.y = e.y;
         xs.ybase = xs.yend = (it.pos - it.first_step) * R;
     }
+    // The first pass only issues (x's round trip overlaps these loads, and
+    // x is paired after them); afterwards each pass computes the step a
+    // buffer holds and refills that buffer with the wave's next step.
     StepBuf buf[NB];
     Step st[NB];
 #pragma unroll
-    for (int i = 0; i < NB; ++i) st[i].lin = -1;
-    // The first pass only issues; afterwards each pass computes the step a
-    // buffer holds and refills that buffer with the wave's next step.
+    for (int i = 0; i < NB; ++i) {
+        st[i] = next_step<R>(it, p, c, lds_counter, lane);
+        issue_from<LPR, GPL>(buf[i], st[i], it.cur, lane);
+    }
+    pair_x<LPR, GPL, MAXG>(xraw, xng, lane, xs.xr);
     for (;;) {
         bool any = false;
 #pragma unroll

@@ -181,19 +181,24 @@ __device__ __forceinline__ void wave_lds_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// x groups of this lane: every group's loads are issued before any is
-// rearranged, so they share one round trip.  Lanes whose group index runs
-// past the row get zeros.
+// x groups of this lane, in two halves so that other loads can be issued
+// between them: load_x_raw issues the loads of every group (one round trip
+// for all), pair_x rearranges them to the dequantized codes' pairing (lanes
+// whose group index runs past the row get zeros), which waits for them.
 template <int LPR, int GPL, int MAXG>
-__device__ __forceinline__ void load_x_lane(const uint16_t* x, int ng, int lane, half2v (&xr)[MAXG][16]) {
+__device__ __forceinline__ void load_x_raw(const uint16_t* x, int ng, int lane, u32x4 (&raw)[MAXG][4]) {
     const int sub = lane & (LPR - 1);
-    u32x4 raw[GPL][4];
 #pragma unroll
     for (int j = 0; j < GPL; ++j) {
         const WQ_GLOBAL u32x4* src = gbl(reinterpret_cast<const u32x4*>(x + (int64_t)min(sub + LPR * j, ng - 1) * kGroup));
 #pragma unroll
         for (int c = 0; c < 4; ++c) raw[j][c] = src[c];
     }
+}
+
+template <int LPR, int GPL, int MAXG>
+__device__ __forceinline__ void pair_x(const u32x4 (&raw)[MAXG][4], int ng, int lane, half2v (&xr)[MAXG][16]) {
+    const int sub = lane & (LPR - 1);
 #pragma unroll
     for (int j = 0; j < GPL; ++j) {
         const bool act = sub + LPR * j < ng;
@@ -206,6 +211,22 @@ __device__ __forceinline__ void load_x_lane(const uint16_t* x, int ng, int lane,
             xr[j][4 * c + 3] = as_h2(act ? (d.y >> 16) | (d.w & 0xFFFF0000u) : 0u);
         }
     }
+}
+
+// Keeps the loads issued so far ahead of any issued later: the compiler
+// may otherwise schedule later loads first (the load counter retires in
+// issue order, so a wait for the earlier loads would then wait for those).
+__device__ __forceinline__ void load_order_fence() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+// Both halves at once, when nothing is to be issued in between.
+template <int LPR, int GPL, int MAXG>
+__device__ __forceinline__ void load_x_lane(const uint16_t* x, int ng, int lane, half2v (&xr)[MAXG][16]) {
+    u32x4 raw[MAXG][4];
+    load_x_raw<LPR, GPL, MAXG>(x, ng, lane, raw);
+    pair_x<LPR, GPL, MAXG>(raw, ng, lane, xr);
 }
 
 // Buffer resources over one linear's codes and scales.  A load's byte offset

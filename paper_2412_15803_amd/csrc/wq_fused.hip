@@ -120,6 +120,7 @@ __device__ __forceinline__ void stage_prologue(const Args& a, uint16_t* s_x, flo
             xb[r] = bs[c];
         }
     }
+    load_order_fence();
     between();
     float inv = 0.0f;
     if (a.prologue == WQ_PROLOGUE_RMSNORM) {
@@ -159,37 +160,6 @@ __device__ __forceinline__ void stage_prologue(const Args& a, uint16_t* s_x, flo
         reinterpret_cast<u32x4*>(s_x)[c] = u32x4{o[0], o[1], o[2], o[3]};
     }
     __syncthreads();
-}
-
-// load_x_lane in two halves, so that other loads can be issued between them
-// without waiting: the raw loads of this lane's groups, then their pairing
-// (lanes whose group index runs past the row get zeros).
-template <int LPR, int GPL>
-__device__ __forceinline__ void x_lane_raw(const uint16_t* x, int ng, int lane, u32x4 (&raw)[GPL][4]) {
-    const int sub = lane & (LPR - 1);
-#pragma unroll
-    for (int j = 0; j < GPL; ++j) {
-        const WQ_GLOBAL u32x4* src = gbl(reinterpret_cast<const u32x4*>(x + (int64_t)min(sub + LPR * j, ng - 1) * kGroup));
-#pragma unroll
-        for (int c = 0; c < 4; ++c) raw[j][c] = src[c];
-    }
-}
-
-template <int LPR, int GPL>
-__device__ __forceinline__ void x_lane_pair(const u32x4 (&raw)[GPL][4], int ng, int lane, half2v (&xr)[GPL][16]) {
-    const int sub = lane & (LPR - 1);
-#pragma unroll
-    for (int j = 0; j < GPL; ++j) {
-        const bool act = sub + LPR * j < ng;
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            const u32x4 d = raw[j][c];
-            xr[j][4 * c + 0] = as_h2(act ? (d.x & 0xFFFFu) | (d.z << 16) : 0u);
-            xr[j][4 * c + 1] = as_h2(act ? (d.x >> 16) | (d.z & 0xFFFF0000u) : 0u);
-            xr[j][4 * c + 2] = as_h2(act ? (d.y & 0xFFFFu) | (d.w << 16) : 0u);
-            xr[j][4 * c + 3] = as_h2(act ? (d.y >> 16) | (d.w & 0xFFFF0000u) : 0u);
-        }
-    }
 }
 
 // load_x_lane with x_eff already in LDS.
@@ -284,10 +254,11 @@ __global__ __launch_bounds__(kBlock) void fused_m1_kernel(const Args a) {
             load_x_lane_lds<LPR, GPL>(s_x, a.ng, lane, xr);
         } else {
             u32x4 raw[GPL][4];
-            x_lane_raw<LPR, GPL>(a.x, a.ng, lane, raw);
+            load_x_raw<LPR, GPL, GPL>(a.x, a.ng, lane, raw);
+            load_order_fence();
             issue_step<LPR, GPL, WQ_FUSED_CPOL, kFLoads>(b0, rs, row_of(0), a.ng, lane);
             issue_step<LPR, GPL, WQ_FUSED_CPOL, kFLoads>(b1, rs, row_of(1), a.ng, lane);
-            x_lane_pair<LPR, GPL>(raw, a.ng, lane, xr);
+            pair_x<LPR, GPL, GPL>(raw, a.ng, lane, xr);
         }
         if (rb >= a.n) return;
         // As in gemv_m1_kernel: unconditional issues, so the wait counts

@@ -114,10 +114,12 @@ __global__ __launch_bounds__(kBlock) void gemv_m1_kernel(const u32x4* packed, co
     __shared__ __align__(16) uint16_t s_y[kWavesPerBlock][kYRows];
     uint16_t* ylds = s_y[threadIdx.x / kWave];
 
-    // x first: its loads are then the oldest in flight, and waiting for
-    // them never waits for a weight load.
-    half2v xr[GPL][16];
-    load_x_lane<LPR, GPL, GPL>(x, ng, lane, xr);
+    // x's loads first, then the first weight steps, then x is paired: the
+    // weights are in flight during x's round trip, and since x's loads are
+    // the oldest, waiting for them never waits for a weight load.
+    u32x4 xraw[GPL][4];
+    load_x_raw<LPR, GPL, GPL>(x, ng, lane, xraw);
+    load_order_fence();
 
     // Every pass issues into every buffer, also past the wave's last step:
     // those loads start at row n, past the end of the codes and scales, and
@@ -129,7 +131,12 @@ __global__ __launch_bounds__(kBlock) void gemv_m1_kernel(const u32x4* packed, co
 #pragma unroll
     for (int i = 0; i < NB; ++i)
         issue_step<LPR, GPL, WQ_M1_CPOL, kM1Loads>(buf[i], rs, i < steps ? rb + i * R : n, ng, lane);
-    for (int64_t s = 0; s < steps; s += NB) {
+    half2v xr[GPL][16];
+    pair_x<LPR, GPL, GPL>(xraw, ng, lane, xr);
+    // steps >= 1 here: a loop that tests first would let the compiler sink
+    // x's loads behind that test, after the weight loads.
+    int64_t s = 0;
+    do {
 #pragma unroll
         for (int i = 0; i < NB; ++i) {
             const int64_t si = s + i;
@@ -141,7 +148,8 @@ __global__ __launch_bounds__(kBlock) void gemv_m1_kernel(const u32x4* packed, co
             issue_step<LPR, GPL, WQ_M1_CPOL, kM1Loads>(buf[i], rs, si + NB < steps ? rb + (si + NB) * R : n, ng,
                                                        lane);
         }
-    }
+        s += NB;
+    } while (s < steps);
     flush_y(y, rb, ylds, (int)(re - rb), lane);
 }
 
