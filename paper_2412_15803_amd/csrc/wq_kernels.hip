@@ -87,6 +87,9 @@ __global__ __launch_bounds__(kBlock) void pack_kernel(const float* __restrict__ 
 #ifndef WQ_M1_CPOL
 #define WQ_M1_CPOL kCpolNonTemporal
 #endif
+#ifndef WQ_M1_X_LDS
+#define WQ_M1_X_LDS 0
+#endif
 #ifndef WQ_M1_WAVES
 #define WQ_M1_WAVES (256 * 4)
 #endif
@@ -106,9 +109,11 @@ __global__ __launch_bounds__(kBlock) void gemv_m1_kernel(const u32x4* packed, co
     // the row bookkeeping stays in scalar registers and branches uniform.
     const int64_t wave = (int64_t)__builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerBlock + threadIdx.x / kWave);
     const int64_t rb = wave * rows_per_wave;
+#if !WQ_M1_X_LDS
     if (rb >= n) return;
+#endif
     const int64_t re = min(n, rb + rows_per_wave);
-    const int64_t steps = (re - rb + R - 1) / R;
+    const int64_t steps = rb < n ? (re - rb + R - 1) / R : 0;
     const LinearRsrc rs = make_rsrc(packed, scales, (uint32_t)(n * ng * 2));
 
     __shared__ __align__(16) uint16_t s_y[kWavesPerBlock][kYRows];
@@ -117,9 +122,26 @@ __global__ __launch_bounds__(kBlock) void gemv_m1_kernel(const u32x4* packed, co
     // x's loads first, then the first weight steps, then x is paired: the
     // weights are in flight during x's round trip, and since x's loads are
     // the oldest, waiting for them never waits for a weight load.
+#if WQ_M1_X_LDS
+    // Variant: x read once per workgroup into LDS (16-byte chunks, thread t
+    // taking chunks t, t + 256, ...), then each wave's lanes read their
+    // groups from there.  Every wave takes part in the barrier.
+    constexpr int kXChunks = LPR * GPL * (kGroup / 8);
+    constexpr int CPT = (kXChunks + kBlock - 1) / kBlock;
+    __shared__ __align__(16) u32x4 s_xk[kXChunks];
+    const int chunks = ng * (kGroup / 8);
+    u32x4 xc[CPT];
+#pragma unroll
+    for (int r = 0; r < CPT; ++r) {
+        const int c = (int)threadIdx.x + kBlock * r;
+        if (c < chunks) xc[r] = gbl(reinterpret_cast<const u32x4*>(x))[c];
+    }
+    load_order_fence();
+#else
     u32x4 xraw[GPL][4];
     load_x_raw<LPR, GPL, GPL>(x, ng, lane, xraw);
     load_order_fence();
+#endif
 
     // Every pass issues into every buffer, also past the wave's last step:
     // those loads start at row n, past the end of the codes and scales, and
@@ -131,6 +153,23 @@ __global__ __launch_bounds__(kBlock) void gemv_m1_kernel(const u32x4* packed, co
 #pragma unroll
     for (int i = 0; i < NB; ++i)
         issue_step<LPR, GPL, WQ_M1_CPOL, kM1Loads>(buf[i], rs, i < steps ? rb + i * R : n, ng, lane);
+#if WQ_M1_X_LDS
+#pragma unroll
+    for (int r = 0; r < CPT; ++r) {
+        const int c = (int)threadIdx.x + kBlock * r;
+        if (c < chunks) s_xk[c] = xc[r];
+    }
+    __syncthreads();
+    if (rb >= n) return;
+    u32x4 xraw[GPL][4];
+    {
+        const int sub = lane & (LPR - 1);
+#pragma unroll
+        for (int j = 0; j < GPL; ++j)
+#pragma unroll
+            for (int c = 0; c < 4; ++c) xraw[j][c] = s_xk[4 * min(sub + LPR * j, ng - 1) + c];
+    }
+#endif
     half2v xr[GPL][16];
     pair_x<LPR, GPL, GPL>(xraw, ng, lane, xr);
     // steps >= 1 here: a loop that tests first would let the compiler sink
