@@ -32,10 +32,14 @@ namespace {
 
 using namespace dev;
 
-// Waves of one workgroup: what a CU holds of the narrow (MAXG <= 4, three
-// waves per SIMD) and the wide variant (two per SIMD).
+// Waves of one workgroup (one workgroup per CU): two per SIMD for the
+// narrow (MAXG <= 4) and the wide variant.  The narrow variant took three
+// per SIMD with three buffers of six-load steps; two per SIMD with two
+// buffers of four-load steps measured faster on the 3B step (272-274 against
+// 281-282 us over 200 steps, alternated on one box) and on one-layer calls
+// (3B 14.4-15.3 against 17.2 us).
 #ifndef WQ_GROUPED_WAVES4
-#define WQ_GROUPED_WAVES4 12
+#define WQ_GROUPED_WAVES4 8
 #endif
 #ifndef WQ_GROUPED_WAVES8
 #define WQ_GROUPED_WAVES8 8
@@ -184,31 +188,32 @@ __device__ __forceinline__ void compute_from(const StepBuf& b, XSlot<MAXG>& xs, 
         }
         xs.ybase = s.row;
     }
-    compute_step<LPR, GPL, MAXG>(b, xs.xr, s.nrows, ylds, s.row - xs.ybase, lane);
+    compute_step<LPR, GPL, MAXG, grouped_step_loads(MAXG)>(b, xs.xr, s.nrows, ylds, s.row - xs.ybase, lane);
     xs.yend = s.row + s.nrows;
 }
 
 // Issues are unconditional: once the wave's work is done it re-loads row 0
 // of its current linear (never computed), so every path through the loop
 // issues the same loads and the compiler's wait counts stay exact.
-template <int LPR, int GPL>
+template <int LPR, int GPL, int MAXG>
 __device__ __forceinline__ void issue_from(StepBuf& b, const Step& s, const LinearRef& l, int lane) {
-    issue_step<LPR, GPL, kCpolNonTemporal>(b, make_rsrc(l.packed, l.scales, l.scale_bytes), s.row, l.ng, lane);
+    issue_step<LPR, GPL, kCpolNonTemporal, grouped_step_loads(MAXG)>(b, make_rsrc(l.packed, l.scales, l.scale_bytes),
+                                                                     s.row, l.ng, lane);
 }
 
 // Register buffers in the pipeline: as many steps as fit a budget of
-// in-flight 16-byte loads per lane (18 beside the narrow kernel's x
-// registers, which keeps three waves per SIMD; 14 beside the wide one's),
-// at least two and at most four.
+// in-flight 16-byte loads per lane (8 in the narrow kernel, which gives the
+// 3B step's K = 3072 and 8192 linears two buffers; 14 beside the wide one's
+// x registers), at least two and at most four.
 #ifndef WQ_DEPTH_BUDGET4
-#define WQ_DEPTH_BUDGET4 18
+#define WQ_DEPTH_BUDGET4 8
 #endif
 #ifndef WQ_DEPTH_BUDGET8
 #define WQ_DEPTH_BUDGET8 14
 #endif
 template <int LPR, int GPL, int MAXG>
 constexpr int pipeline_depth() {
-    constexpr int per_step = StepShape<LPR, GPL>::U * GPL;
+    constexpr int per_step = StepShape<LPR, GPL, grouped_step_loads(MAXG)>::U * GPL;
     constexpr int nb = (MAXG <= 4 ? WQ_DEPTH_BUDGET4 : WQ_DEPTH_BUDGET8) / per_step;
     return nb < 2 ? 2 : (nb > 4 ? 4 : nb);
 }
@@ -229,7 +234,7 @@ template <int LPR, int GPL, int MAXG>
 __device__ __forceinline__ void run_block(const DecodePlan& p, const DecodeClass& c, const DecodeBlock& b,
                                           uint32_t* lds_counter, int wave, int waves, uint16_t* ylds, int lane) {
     constexpr int NB = pipeline_depth<LPR, GPL, MAXG>();
-    constexpr int R = StepShape<LPR, GPL>::ROWS;
+    constexpr int R = StepShape<LPR, GPL, grouped_step_loads(MAXG)>::ROWS;
     static_assert(2 * NB * R <= kYRows, "a chunk's rows fit the wave's staging slice");
     StepIter it;
     it.begin = b.begin;
@@ -271,7 +276,7 @@ __device__ __forceinline__ void run_block(const DecodePlan& p, const DecodeClass
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
         st[i] = next_step<R>(it, p, c, lds_counter, lane);
-        issue_from<LPR, GPL>(buf[i], st[i], it.cur, lane);
+        issue_from<LPR, GPL, MAXG>(buf[i], st[i], it.cur, lane);
     }
     pair_x<LPR, GPL, MAXG>(xraw, xng, lane, xs.xr);
     for (;;) {
@@ -281,7 +286,7 @@ __device__ __forceinline__ void run_block(const DecodePlan& p, const DecodeClass
             compute_from<LPR, GPL, MAXG>(buf[i], xs, st[i], p, ylds, lane);
             st[i] = next_step<R>(it, p, c, lds_counter, lane);
             any = any || st[i].lin >= 0;
-            issue_from<LPR, GPL>(buf[i], st[i], it.cur, lane);
+            issue_from<LPR, GPL, MAXG>(buf[i], st[i], it.cur, lane);
         }
         if (!any) break;
     }
@@ -295,8 +300,7 @@ __device__ __forceinline__ void run_block(const DecodePlan& p, const DecodeClass
 
 // The plan arrays arrive as separate read-only, non-aliasing arguments, so
 // every table read is a scalar load with a wave-uniform value.  One
-// workgroup per CU: three waves per SIMD fit the narrow variant without
-// spilling, the wide one (up to eight groups of x per lane) stays at two.
+// workgroup per CU, two waves per SIMD (cu_waves).
 template <int MAXG>
 __global__ __launch_bounds__(cu_waves(MAXG) * kWave, cu_waves(MAXG) / 4) void grouped_m1_kernel(
     const DecodeEntry* __restrict__ entries, const DecodeClass* __restrict__ classes,

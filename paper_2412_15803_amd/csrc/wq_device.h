@@ -146,14 +146,29 @@ __device__ __forceinline__ float segment_sum(float v) {
 // A "step" is U rows per slot (U * 64/LPR rows per wave) and U * GPL loads
 // per lane; slot s takes rows row0 + s*U .. row0 + s*U + U - 1.
 // Loads of 16 bytes per lane in one step (rows per slot = this / GPL, at
-// least one).  Six measured best on the 3B- and 8B-class decode steps: the
-// 8B step's K=4096 linears then take three rows per slot.
+// least one), by default.  Six measured best on the 8B-class decode step
+// (whose K=4096 linears then take three rows per slot, in the step kernel's
+// wide variant); the narrow variant and the single-linear kernels take
+// fewer.
 #ifndef WQ_STEP_LOADS
 #define WQ_STEP_LOADS 6
 #endif
 
 __host__ __device__ constexpr int step_rows_per_slot(int gpl, int loads = WQ_STEP_LOADS) {
     return gpl >= loads ? 1 : loads / gpl;
+}
+
+// Loads per step of the batch-1 step kernel's narrow variant (up to four
+// groups of x per lane) and its wide variant; its plans number steps with
+// the same counts.
+#ifndef WQ_GROUPED_LOADS4
+#define WQ_GROUPED_LOADS4 4
+#endif
+#ifndef WQ_GROUPED_LOADS8
+#define WQ_GROUPED_LOADS8 WQ_STEP_LOADS
+#endif
+__host__ __device__ constexpr int grouped_step_loads(int max_gpl) {
+    return max_gpl <= 4 ? WQ_GROUPED_LOADS4 : WQ_GROUPED_LOADS8;
 }
 
 // A kernel may take steps of fewer loads (LOADS, at most 8) than the decode

@@ -13,7 +13,11 @@ namespace {
 
 size_t align16(size_t v) { return (v + 15) & ~size_t(15); }
 
-int rows_per_step(int lpr, int gpl) { return dev::step_rows_per_slot(gpl) * (64 / lpr); }
+// Rows per step of a batch-1 grouped launch whose widest linear has
+// `max_gpl` groups of x per lane (the kernel variant it runs on).
+int rows_per_step(int lpr, int gpl, int max_gpl) {
+    return dev::step_rows_per_slot(gpl, dev::grouped_step_loads(max_gpl)) * (64 / lpr);
+}
 
 void fill_entry(DecodeEntry& e, const wq_linear& l) {
     e = DecodeEntry{};
@@ -49,17 +53,21 @@ GroupPlan plan_group(const wq_linear* lin, const Group& g, int capacity4, int ca
     double work[kMaxClasses] = {};
     int ncls = 0, max_gpl = 1;
     for (int i = 0; i < count; ++i) {
+        int lpr = 64, gpl = 1;
+        dev::pick_shape((int)(lin[g.begin + i].K / 32), lpr, gpl);
+        max_gpl = std::max(max_gpl, gpl);
+    }
+    for (int i = 0; i < count; ++i) {
         const wq_linear& l = lin[g.begin + i];
         int lpr = 64, gpl = 1;
         dev::pick_shape((int)(l.K / 32), lpr, gpl);
-        max_gpl = std::max(max_gpl, gpl);
         int c = class_of(cls, ncls, lpr, gpl);
         if (c < 0) {
             c = ncls++;  // pick_shape returns at most kMaxClasses distinct shapes
             cls[c].lpr = lpr;
             cls[c].gpl = gpl;
         }
-        const int r = rows_per_step(lpr, gpl);
+        const int r = rows_per_step(lpr, gpl, max_gpl);
         cls[c].steps += (l.N + r - 1) / r;
         cls[c].count += 1;
         work[c] += (double)l.N * ((double)(l.K / 2 + l.K / 16) + kRowCost);
@@ -104,7 +112,7 @@ GroupPlan plan_group(const wq_linear* lin, const Group& g, int capacity4, int ca
         e.lpr = lpr;
         e.gpl = gpl;
         const int c = class_of(cls, ncls, lpr, gpl);
-        const int r = rows_per_step(lpr, gpl);
+        const int r = rows_per_step(lpr, gpl, max_gpl);
         e.steps = (e.n + r - 1) / r;
         e.first_step = next_step[c];
         next_step[c] += e.steps;
