@@ -216,9 +216,11 @@ __host__ __device__ constexpr int block_lds_bytes(int t, int sm, int waves) {
 // j = 2 tt + h of a pair is tile tt at step 2 p + h, so the two items that
 // read one 128-byte run of each row (eight groups) are issued back to back
 // (issuing all tiles of one step before the next step's measured 1.5x
-// slower).  Eight register buffers hold the items in flight: the two items
-// of a tile are computed, then their buffers are refilled with the items
-// eight on, so three to four tiles' pairs of loads are always in flight.  x
+// slower).  kDepth register buffers (four) hold the items in flight: the
+// two items of a tile are computed, then their buffers are refilled with
+// the items kDepth on, so one to two tiles' pairs of loads are always in
+// flight (eight buffers, the first version, were 1-4% slower on the 3B and
+// 8B steps at M = 4, 8 and 16; two, 9-15% slower).  x
 // of the next pair is loaded right after the current pair's x is unpacked,
 // ahead of that pair's weight loads, and unpacked when the pair starts.
 // Loads past the wave's range re-read its last pair (already in the caches)
@@ -226,7 +228,7 @@ __host__ __device__ constexpr int block_lds_bytes(int t, int sm, int waves) {
 // fixed order and one wave per tile rounds and stores it.  `lds` is the
 // block's dynamic LDS, wave_lds_bytes(T, SM) per wave.
 #ifndef WQ_MFMA_DEPTH
-#define WQ_MFMA_DEPTH 8
+#define WQ_MFMA_DEPTH 4
 #endif
 constexpr int kDepth = WQ_MFMA_DEPTH;
 
@@ -411,6 +413,16 @@ hipError_t launch_t(const uint32_t* packed, const uint16_t* scales, const uint16
     return hipGetLastError();
 }
 
+// A single linear's K is split among a block's waves at about this many
+// steps per wave (up to four waves): at 8 (four waves for K = 4096) the 8B
+// qkv, o and gate_up linears took 9.0, 6.8 and 18.5-20.6 us at M = 4-16,
+// against 11.3-11.5, 9.0 and 20.7-23.1 us at 16 (two waves).
+#ifndef WQ_MFMA_SPLIT_STEPS
+#define WQ_MFMA_SPLIT_STEPS 8
+#endif
+#ifndef WQ_MFMA_TARGET_WAVES
+#define WQ_MFMA_TARGET_WAVES 1536
+#endif
 #ifndef WQ_MFMA_TILES
 #define WQ_MFMA_TILES 8
 #endif
@@ -435,12 +447,13 @@ hipError_t launch_gemm_mfma(const uint32_t* packed, const uint16_t* scales, cons
                             int64_t n, int64_t k, int64_t m, hipStream_t stream) {
     const int64_t ng = k / kGroup;
     const int64_t nsteps = (ng + 3) / 4;
-    // Waves per block: about 16 steps each where K allows, at most 4.
-    const int w = (int)std::min<int64_t>(grouped_mfma_max_waves(), std::max<int64_t>(1, nsteps / 16));
+    // Waves per block: about WQ_MFMA_SPLIT_STEPS steps each where K allows,
+    // at most 4.
+    const int w = (int)std::min<int64_t>(grouped_mfma_max_waves(), std::max<int64_t>(1, nsteps / WQ_MFMA_SPLIT_STEPS));
     // Tiles per block: as many (up to 8, sharing each x load) as still keep
-    // about 1536 waves in flight.
+    // about WQ_MFMA_TARGET_WAVES waves in flight.
     int t = WQ_MFMA_TILES;
-    while (t > 1 && (n + 16 * t - 1) / (16 * t) * w < 1536) t /= 2;
+    while (t > 1 && (n + 16 * t - 1) / (16 * t) * w < WQ_MFMA_TARGET_WAVES) t /= 2;
     for (int64_t m0 = 0; m0 < m; m0 += 16) {
         const int mc = (int)std::min<int64_t>(16, m - m0);
         const uint16_t* xc = x + m0 * k;
