@@ -171,6 +171,20 @@ def test_gemv_integer_exact_m1(n, k):
     _gemv_case(p, s, x, sample_rows(n, 512, 9), True, "integer-exact")
 
 
+# Batch-1 single-linear launches of about 1024 waves: a last wave with one
+# row or one partial step, a wave count just past 1024, and rows that fit
+# one step of the widest shapes.
+M1_LAUNCH_EDGES = [(2049, 3072), (1025, 4096), (2047, 8192), (3, 14336), (65, 96), (1024 * 6 + 5, 3072)]
+
+
+@pytest.mark.parametrize("n,k", M1_LAUNCH_EDGES, ids=lambda v: str(v))
+def test_gemv_integer_exact_m1_launch_edges(n, k):
+    p = wl.random_words_host(n * 11 + k, n, k)
+    s = wl.constant_scales_host(n, k, 0x2400)
+    x = wl.small_int_x_host(n * 5 + k, 1, k)
+    _gemv_case(p, s, x, None, True, "integer-exact launch edge")
+
+
 @pytest.mark.parametrize("n,k", SHAPES_8B + SHAPES_EDGE[2:5], ids=lambda v: str(v))
 @pytest.mark.parametrize("m", [2, 4, 8, 16])
 def test_gemv_integer_exact_small_batch(n, k, m):
