@@ -20,10 +20,14 @@
 // log2 units), l = sum 2^(a - m) and acc = sum 2^(a - m) V over its 8 dims,
 // rescaled once per block.
 //
-// Merging.  The four row states of a wave are merged across lanes, the four
-// wave states through LDS.  With one chunk per sequence the workgroup then
-// writes the fp16 output; otherwise it writes (m, l, acc) to the workspace
-// and merge_kernel combines the chunks of every (sequence, query head).
+// Merging.  The four row states of a wave are merged across lanes with
+// v_permlane16/32_swap exchanges, the four wave states through LDS.  With
+// one chunk per sequence the workgroup then writes the fp16 output;
+// otherwise it writes (m, l, acc) to the workspace and merge_kernel combines
+// the chunks of every (sequence, query head) in a second launch.  When the
+// (sequence, kv head) pairs divide evenly over the XCDs, all chunks of a pair
+// and the merge of its heads run on one XCD, so the merge finds the partial
+// results in that XCD's L2.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 #include <math.h>
@@ -59,6 +63,9 @@ constexpr int kMaxChunk = 4096;
 constexpr int kMaxSplits = 1024;
 static_assert(WQ_ATTN_MAX_SEQ_LEN / kMaxChunk <= kMaxSplits, "chunks per sequence stay bounded");
 constexpr uint16_t kHalfNaN = 0x7E00;
+// Workgroups of a launch are dealt to the XCDs in turn (workgroup b runs on
+// XCD b % kXcds), and each XCD has its own L2.
+constexpr int kXcds = 8;
 
 static_assert(kD == 128, "the lane layout assumes 16 lanes x 8 dims per token");
 
@@ -81,6 +88,7 @@ struct Params {
     int32_t max_seq_len;
     int32_t pages_per_chunk;  // block-table entries one chunk can use
     int32_t pages_lds;        // bytes of LDS before the wave states
+    int32_t xcd_local;        // nonzero: pairs are placed by XCD (xcd_pair)
     float c;            // scale * log2(e): scores in log2 units
 };
 
@@ -121,18 +129,46 @@ struct State {
     float m, l, acc[8];
 };
 
-// Merge the state of the lane `off` positions away (xor) into this one.
-__device__ __forceinline__ void merge_lanes(State& st, int off) {
-    const float m2 = __shfl_xor(st.m, off);
-    const float l2 = __shfl_xor(st.l, off);
-    const float mx = fmaxf(st.m, m2);
+// Fold the states of the two lanes of a pair into one, the pair being lanes
+// l and l ^ 16 (kHalves false) or l and l ^ 32 (kHalves true).
+// v_permlane16_swap of a register with itself hands each lane the values of
+// the even and odd 16-lane row of its pair, v_permlane32_swap those of the
+// lower and upper 32 lanes, so both lanes merge the same two states in the
+// same order (lower first) and end with the same bits.  Both are VALU
+// exchanges: no LDS round trip per value.
+template <bool kHalves>
+__device__ __forceinline__ void pair_values(float x, float& lo, float& hi) {
+    const uint32_t b = __builtin_bit_cast(uint32_t, x);
+    uint32_t e0, e1;
+    // (Non-const results: with `const auto` this compiler reads element 0
+    // for both elements of the returned pair.)
+    if constexpr (kHalves) {
+        auto p = __builtin_amdgcn_permlane32_swap(b, b, false, false);
+        e0 = p[0];
+        e1 = p[1];
+    } else {
+        auto p = __builtin_amdgcn_permlane16_swap(b, b, false, false);
+        e0 = p[0];
+        e1 = p[1];
+    }
+    lo = __builtin_bit_cast(float, e0);
+    hi = __builtin_bit_cast(float, e1);
+}
+
+template <bool kHalves>
+__device__ __forceinline__ void fold_pair(State& st) {
+    float m0, m1, l0, l1;
+    pair_values<kHalves>(st.m, m0, m1);
+    pair_values<kHalves>(st.l, l0, l1);
+    const float mx = fmaxf(m0, m1);
     const float ms = mx == -INFINITY ? 0.0f : mx;
-    const float w1 = exp2_(st.m - ms), w2 = exp2_(m2 - ms);
-    st.l = st.l * w1 + l2 * w2;
+    const float w0 = exp2_(m0 - ms), w1 = exp2_(m1 - ms);
+    st.l = fmaf(l1, w1, l0 * w0);
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-        const float a2 = __shfl_xor(st.acc[e], off);
-        st.acc[e] = st.acc[e] * w1 + a2 * w2;
+        float a0, a1;
+        pair_values<kHalves>(st.acc[e], a0, a1);
+        st.acc[e] = fmaf(a1, w1, a0 * w0);
     }
     st.m = mx;
 }
@@ -146,8 +182,19 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const Params p) {
     float* sh_l = sh_m + kWaves * G;
 
     const int tid = threadIdx.x;
-    const int chunk = blockIdx.x % p.splits;
-    const int seq_kv = blockIdx.x / p.splits;
+    // (sequence, kv head) pair and chunk of this workgroup.  With xcd_local
+    // the pairs are dealt to the XCDs and every chunk of a pair runs on its
+    // pair's XCD, as does the merge of its heads, so the merge reads the
+    // partial results from that XCD's L2 instead of from memory.
+    int chunk, seq_kv;
+    if (p.xcd_local) {
+        const int x = blockIdx.x % kXcds, i = blockIdx.x / kXcds;
+        seq_kv = x + kXcds * (i / p.splits);
+        chunk = i % p.splits;
+    } else {
+        chunk = blockIdx.x % p.splits;
+        seq_kv = blockIdx.x / p.splits;
+    }
     const int kvh = seq_kv % p.hkv;
     const int s = seq_kv / p.hkv;
     const int64_t head0 = (int64_t)s * p.hq + (int64_t)kvh * G;  // first query head of the group
@@ -293,9 +340,13 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const Params p) {
     // Merge the four rows of the wave, then the four waves.
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-        merge_lanes(st[g], 16);
-        merge_lanes(st[g], 32);
+        fold_pair<false>(st[g]);
+        fold_pair<true>(st[g]);
     }
+    // A wave that met a page number outside the cache stores a NaN sum, which
+    // every later fold carries into the output (fmaf(NaN, w, .) is NaN for
+    // any weight), so one plain barrier does instead of a reduction.
+    const bool wave_bad = __builtin_amdgcn_ballot_w64(bad != 0) != 0;
     if (row == 0) {
 #pragma unroll
         for (int g = 0; g < G; ++g) {
@@ -304,11 +355,11 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const Params p) {
             *reinterpret_cast<float4*>(dst + 4) = make_float4(st[g].acc[4], st[g].acc[5], st[g].acc[6], st[g].acc[7]);
             if (col == 0) {
                 sh_m[wave * G + g] = st[g].m;
-                sh_l[wave * G + g] = st[g].l;
+                sh_l[wave * G + g] = wave_bad ? NAN : st[g].l;
             }
         }
     }
-    const int any_bad = __syncthreads_or(bad);
+    __syncthreads();
     for (int i = tid; i < G * kD; i += kThreads) {
         const int g = i / kD, d = i % kD;
         float mx = -INFINITY;
@@ -322,11 +373,11 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const Params p) {
             acc = fmaf(sh_acc[(w * G + g) * kD + d], wt, acc);
         }
         if (p.splits == 1) {
-            p.out[(head0 + g) * kD + d] = any_bad ? kHalfNaN : to_half_bits(acc / l);
+            p.out[(head0 + g) * kD + d] = l != l ? kHalfNaN : to_half_bits(acc / l);
         } else {
             const int64_t slot = (head0 + g) * p.splits + chunk;
             p.part_acc[slot * kD + d] = acc;
-            if (d == 0) p.part_ml[slot] = make_float2(mx, any_bad ? NAN : l);
+            if (d == 0) p.part_ml[slot] = make_float2(mx, l);
         }
     }
 }
@@ -347,7 +398,13 @@ __global__ __launch_bounds__(kThreads) void merge_kernel(const Params p) {
 
     const int tid = threadIdx.x;
     const int slot = tid / kCols, cq = tid % kCols;
-    const int64_t head = blockIdx.x;  // seq * hq + h
+    int64_t head = blockIdx.x;  // seq * hq + h
+    if (p.xcd_local) {  // the heads of pair x + 8 j run on XCD x
+        const int group = p.hq / p.hkv;
+        const int x = blockIdx.x % kXcds, i = blockIdx.x / kXcds;
+        const int pair = x + kXcds * (i / group);
+        head = (int64_t)(pair / p.hkv) * p.hq + (int64_t)(pair % p.hkv) * group + i % group;
+    }
     const int s = (int)(head / p.hq);
     uint16_t* o = p.out + head * kD;
     const float2* ml = p.part_ml + head * p.splits;
@@ -427,6 +484,11 @@ struct Plan {
     size_t ml_offset;  // bytes of part_acc
     size_t ws_bytes;
 };
+
+bool xcd_placement() {
+    const char* e = getenv("WQ_ATTN_XCD_LOCAL");
+    return !e || strtol(e, nullptr, 10) != 0;
+}
 
 int64_t target_blocks() {
     const char* e = getenv("WQ_ATTN_TARGET_BLOCKS");
@@ -623,6 +685,8 @@ wq_status wq_paged_attention(const uint16_t* q, const uint16_t* k_cache, const u
     p.pages_per_chunk = (int32_t)pages_per_chunk;
     p.pages_lds = (int32_t)((pages_per_chunk * 4 + 15) / 16 * 16);
     p.c = (float)((double)scale * 1.4426950408889634);  // log2(e)
+    // Place pairs by XCD only when every XCD gets the same number of them.
+    p.xcd_local = pl.splits > 1 && (num_seqs * num_kv_heads) % kXcds == 0 && xcd_placement();
 
     (void)hipGetLastError();
     const hipError_t e = launch(p, group, num_seqs, static_cast<hipStream_t>(stream));
