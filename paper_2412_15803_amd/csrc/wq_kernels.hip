@@ -209,6 +209,13 @@ __global__ __launch_bounds__(kBlock) void gemv_m1_kernel(const u32x4* packed, co
 constexpr int kMbRows = 256;
 constexpr int kMbU = 4;
 constexpr int kMbStep = 2 * kMbU;  // grouped plans: rows per wave are a multiple of a step of either tiling
+// Waves a single small-batch linear aims for: one per SIMD (2 to 12% faster
+// than the 2048-wave split at M = 2 on the 8B-class shapes, 512 and 2048
+// slower).
+#ifndef WQ_MB_SINGLE_WAVES
+#define WQ_MB_SINGLE_WAVES (256 * 4)
+#endif
+constexpr int64_t kMbSingleWaves = WQ_MB_SINGLE_WAVES;
 
 template <int MB>
 struct MbBuf {
@@ -461,18 +468,22 @@ __global__ __launch_bounds__(kBlock) void grouped_mb_kernel(const DecodeEntry* _
 template <int MB>
 hipError_t launch_mb(const uint32_t* packed, const uint16_t* scales, const uint16_t* x, uint16_t* y, int64_t n,
                      int64_t ng, int m, hipStream_t stream) {
-    // Rows per wave in whole steps of the row's tiling (4 rows with 64-group
-    // tiles, 8 with two row sets), about kTargetWaves waves.
+    // x is loaded once per K tile and wave, so the rows a wave owns set how
+    // many weight bytes each x load serves (with 4 rows and 4 batch rows, x
+    // is 3.5x the weight bytes).  So: as many rows per wave, in whole steps
+    // of the row's tiling (4 rows with 64-group tiles, 8 with two row sets),
+    // as leave about kMbSingleWaves waves once each row run's K tiles are
+    // split over up to 4 waves (two tiles each at least).
     const int64_t r = mb_two_sets(ng) ? 2 * kMbU : kMbU;
     const int64_t steps = (n + r - 1) / r;
-    const int64_t spw = min((steps + kTargetWaves - 1) / kTargetWaves, (int64_t)kMbRows / r);
+    const int64_t ntiles = mb_two_sets(ng) ? (ng + 31) / 32 : (ng + 63) / 64;
+    int64_t max_split = 1;
+    while (max_split < 4 && ntiles >= 2 * max_split) max_split *= 2;
+    const int64_t spw = std::max<int64_t>(1, std::min<int64_t>(steps * max_split / kMbSingleWaves, kMbRows / r));
     const int64_t rows_per_wave = spw * r;
     const int64_t runs = (n + rows_per_wave - 1) / rows_per_wave;
-    // Too few row runs to give every SIMD two waves: split each run's K
-    // tiles over 2 or 4 waves (at least one tile each).
-    const int64_t ntiles = mb_two_sets(ng) ? (ng + 31) / 32 : (ng + 63) / 64;
     int split = 1;
-    while (split < 4 && runs * split < 2048 && ntiles >= 2 * split) split *= 2;
+    while (split < max_split && runs * split < kMbSingleWaves) split *= 2;
     const int64_t blocks = (runs * split + kWavesPerBlock - 1) / kWavesPerBlock;
     hipLaunchKernelGGL((gemv_mb_kernel<MB>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, packed, scales, x, y,
                        n, (int)ng, m, rows_per_wave, split);
