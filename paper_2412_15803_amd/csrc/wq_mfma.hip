@@ -420,8 +420,15 @@ hipError_t launch_t(const uint32_t* packed, const uint16_t* scales, const uint16
 #ifndef WQ_MFMA_SPLIT_STEPS
 #define WQ_MFMA_SPLIT_STEPS 8
 #endif
+// Waves a single linear's launch aims for, and the fewest that two tiles per
+// block may leave (8B qkv at M = 4 / 8 / 16: one tile and 1536 waves 9.0 /
+// 9.1 / 10.7 us, two tiles and 768 waves 8.4 / 8.3 / 8.4 us; the 8B and 3B
+// gate_up linears lose 4-12% below 1536 waves).
 #ifndef WQ_MFMA_TARGET_WAVES
 #define WQ_MFMA_TARGET_WAVES 1536
+#endif
+#ifndef WQ_MFMA_MIN_WAVES
+#define WQ_MFMA_MIN_WAVES 768
 #endif
 #ifndef WQ_MFMA_TILES
 #define WQ_MFMA_TILES 8
@@ -451,9 +458,12 @@ hipError_t launch_gemm_mfma(const uint32_t* packed, const uint16_t* scales, cons
     // at most 4.
     const int w = (int)std::min<int64_t>(grouped_mfma_max_waves(), std::max<int64_t>(1, nsteps / WQ_MFMA_SPLIT_STEPS));
     // Tiles per block: as many (up to 8, sharing each x load) as still keep
-    // about WQ_MFMA_TARGET_WAVES waves in flight.
+    // about WQ_MFMA_TARGET_WAVES waves in flight, but two while that leaves
+    // at least WQ_MFMA_MIN_WAVES: with one tile, a step's x (up to 16 batch
+    // rows) serves only 16 weight rows, up to 3.6 times their bytes.
+    auto waves = [&](int tiles) { return (n + 16 * tiles - 1) / (16 * tiles) * w; };
     int t = WQ_MFMA_TILES;
-    while (t > 1 && (n + 16 * t - 1) / (16 * t) * w < WQ_MFMA_TARGET_WAVES) t /= 2;
+    while (t > 1 && waves(t) < WQ_MFMA_TARGET_WAVES && !(t == 2 && waves(2) >= WQ_MFMA_MIN_WAVES)) t /= 2;
     for (int64_t m0 = 0; m0 < m; m0 += 16) {
         const int mc = (int)std::min<int64_t>(16, m - m0);
         const uint16_t* xc = x + m0 * k;
