@@ -413,27 +413,36 @@ hipError_t launch_t(const uint32_t* packed, const uint16_t* scales, const uint16
     return hipGetLastError();
 }
 
-// A single linear's K is split among a block's waves at about this many
-// steps per wave (up to four waves): at 8 (four waves for K = 4096) the 8B
-// qkv, o and gate_up linears took 9.0, 6.8 and 18.5-20.6 us at M = 4-16,
-// against 11.3-11.5, 9.0 and 20.7-23.1 us at 16 (two waves).
+// A single linear's launch (measured over the 3B and 8B decode shapes at
+// M = 4, 8, 16, with every waves-per-block / tiles-per-block pair forced):
+// - K is split among a block's waves, a power of two up to four, with at
+//   least WQ_MFMA_SPLIT_STEPS steps each: blocks of three waves (the 3B
+//   shapes at 8 steps a wave) were 5-11% slower than blocks of four.
+// - Tiles per block: as many as keep WQ_MFMA_TARGET_WAVES waves, but two
+//   while that leaves WQ_MFMA_MIN_WAVES; with one tile a step's x (up to 16
+//   batch rows) serves only 16 weight rows.
+// - One tile per block at most 8 batch rows and at least
+//   WQ_MFMA_WIDE_MIN_STEPS steps: eight waves per block (8B down at M = 4
+//   15.9 -> 13.3 us, 3B down 10.0 -> 8.5 us; at M = 16 four waves stay
+//   faster).
 #ifndef WQ_MFMA_SPLIT_STEPS
-#define WQ_MFMA_SPLIT_STEPS 8
+#define WQ_MFMA_SPLIT_STEPS 6
 #endif
-// Waves a single linear's launch aims for, and the fewest that two tiles per
-// block may leave (8B qkv at M = 4 / 8 / 16: one tile and 1536 waves 9.0 /
-// 9.1 / 10.7 us, two tiles and 768 waves 8.4 / 8.3 / 8.4 us; the 8B and 3B
-// gate_up linears lose 4-12% below 1536 waves).
 #ifndef WQ_MFMA_TARGET_WAVES
-#define WQ_MFMA_TARGET_WAVES 1536
+#define WQ_MFMA_TARGET_WAVES 1024
 #endif
 #ifndef WQ_MFMA_MIN_WAVES
-#define WQ_MFMA_MIN_WAVES 768
+#define WQ_MFMA_MIN_WAVES 640
+#endif
+#ifndef WQ_MFMA_WIDE_MIN_STEPS
+#define WQ_MFMA_WIDE_MIN_STEPS 32
 #endif
 #ifndef WQ_MFMA_TILES
 #define WQ_MFMA_TILES 8
 #endif
 constexpr int kGroupedTiles = WQ_MFMA_TILES;
+constexpr int kSplitWaves = 4;      // waves that split K in a block
+constexpr int kWideSplitWaves = 8;  // the same for one-tile single linears (the kernels take 512 threads)
 
 }  // namespace
 
@@ -441,7 +450,7 @@ int grouped_mfma_tiles() { return kGroupedTiles; }
 
 // Four waves' scale-window slots (16 KiB each with eight tiles) fill the
 // 64 KiB a launch may ask for without raising its limit.
-int grouped_mfma_max_waves() { return 4; }
+int grouped_mfma_max_waves() { return kSplitWaves; }
 
 hipError_t launch_grouped_mfma(const DecodeEntry* entries, int count, int64_t blocks, int waves_per_block,
                                int64_t m0, int m, hipStream_t stream) {
@@ -454,26 +463,22 @@ hipError_t launch_gemm_mfma(const uint32_t* packed, const uint16_t* scales, cons
                             int64_t n, int64_t k, int64_t m, hipStream_t stream) {
     const int64_t ng = k / kGroup;
     const int64_t nsteps = (ng + 3) / 4;
-    // Waves per block: about WQ_MFMA_SPLIT_STEPS steps each where K allows,
-    // at most 4.
-    const int w = (int)std::min<int64_t>(grouped_mfma_max_waves(), std::max<int64_t>(1, nsteps / WQ_MFMA_SPLIT_STEPS));
-    // Tiles per block: as many (up to 8, sharing each x load) as still keep
-    // about WQ_MFMA_TARGET_WAVES waves in flight, but two while that leaves
-    // at least WQ_MFMA_MIN_WAVES: with one tile, a step's x (up to 16 batch
-    // rows) serves only 16 weight rows, up to 3.6 times their bytes.
+    int w = 1;
+    while (w < grouped_mfma_max_waves() && nsteps / (2 * w) >= WQ_MFMA_SPLIT_STEPS) w *= 2;
     auto waves = [&](int tiles) { return (n + 16 * tiles - 1) / (16 * tiles) * w; };
     int t = WQ_MFMA_TILES;
     while (t > 1 && waves(t) < WQ_MFMA_TARGET_WAVES && !(t == 2 && waves(2) >= WQ_MFMA_MIN_WAVES)) t /= 2;
     for (int64_t m0 = 0; m0 < m; m0 += 16) {
         const int mc = (int)std::min<int64_t>(16, m - m0);
+        const int wc = t == 1 && mc <= 8 && nsteps >= WQ_MFMA_WIDE_MIN_STEPS ? kWideSplitWaves : w;
         const uint16_t* xc = x + m0 * k;
         uint16_t* yc = y + m0 * n;
         hipError_t e = hipSuccess;
         switch (t) {
-            case 8: e = launch_t<8>(packed, scales, xc, yc, n, ng, mc, w, stream); break;
-            case 4: e = launch_t<4>(packed, scales, xc, yc, n, ng, mc, w, stream); break;
-            case 2: e = launch_t<2>(packed, scales, xc, yc, n, ng, mc, w, stream); break;
-            default: e = launch_t<1>(packed, scales, xc, yc, n, ng, mc, w, stream); break;
+            case 8: e = launch_t<8>(packed, scales, xc, yc, n, ng, mc, wc, stream); break;
+            case 4: e = launch_t<4>(packed, scales, xc, yc, n, ng, mc, wc, stream); break;
+            case 2: e = launch_t<2>(packed, scales, xc, yc, n, ng, mc, wc, stream); break;
+            default: e = launch_t<1>(packed, scales, xc, yc, n, ng, mc, wc, stream); break;
         }
         if (e != hipSuccess) return e;
     }
