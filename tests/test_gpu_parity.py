@@ -287,6 +287,18 @@ def test_gemv_pow2_scales_matrix_cores_bit_exact(n, k, m):
     _gemv_case(p, s, x, None, True, "power-of-two scales")
 
 
+# Batches past 16 rows run on the matrix cores in chunks of 16 rows.  On a
+# one-tile launch with at least 32 steps of K, a last chunk of at most 8 rows
+# splits K over eight waves per block and the chunks before it over four.
+@pytest.mark.parametrize("n,k,m", [(300, 4096, 20), (4096, 4096, 24), (131, 14336, 40), (1000, 8192, 56)],
+                         ids=lambda v: str(v))
+def test_gemv_integer_exact_matrix_core_chunks(n, k, m):
+    p = wl.random_words_host(n * 13 + k + m, n, k)
+    s = wl.constant_scales_host(n, k, 0x2400)
+    x = wl.small_int_x_host(n + 11 * k + m, m, k)
+    _gemv_case(p, s, x, sample_rows(n, 256, 23), True, "integer-exact chunked batch")
+
+
 @pytest.mark.parametrize("path", ["vector", "default"])
 @pytest.mark.parametrize("n,k,m", _random_small_batch_shapes(24, 2024), ids=lambda v: str(v))
 def test_gemv_integer_exact_small_batch_random_shapes(n, k, m, path, monkeypatch):
