@@ -20,7 +20,7 @@ import glob
 import os
 import statistics
 
-from .build import source_hash
+from .build import STEP_KERNEL_SOURCES, source_hash
 
 
 def _rows(directory, pattern):
@@ -89,8 +89,8 @@ def summarise(args):
         _, _, fb, wb = _traffic(fetch, write, f_scale, w_scale, k)
         others.append(f"| other kernel `{k}`: launches, avg duration (us), scaled fetch + write bytes | "
                       f"{len(d)}, {statistics.mean(d):.2f}, {fb:,.0f} + {wb:,.0f} |")
-    names = tuple(args.sources.split(",")) if args.sources else None
-    src_hash = source_hash(names) if names else source_hash()
+    names = tuple(args.sources.split(",")) if args.sources else STEP_KERNEL_SOURCES
+    src_hash = source_hash(names)
     lines = [
         f"# {args.title}",
         "",
@@ -128,6 +128,7 @@ def summarise(args):
         "",
         "```",
         f"source_hash: {src_hash}",
+        f"source_files: {','.join(names)}",
         f"traffic_bytes_per_launch: {traffic:.0f}",
         f"avg_duration_us: {avg:.3f}",
         f"median_duration_us: {med:.3f}",
