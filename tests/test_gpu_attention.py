@@ -219,6 +219,23 @@ def test_attention_invalid_tables_give_nan(max_len):
     assert np.array_equal(ok.view(np.uint16), clean.view(np.uint16))
 
 
+@pytest.mark.parametrize("hq,lens", [(24, (4096,)), (32, (3000, 7, 5000, 64)), (24, (2048,) * 16)])
+def test_attention_xcd_placement_bit_identical(hq, lens, monkeypatch):
+    """Placing every chunk of a (sequence, kv head) pair on one XCD only
+    moves work between workgroups: each chunk still covers the same tokens
+    and the merge folds the chunks in the same order, so the outputs are
+    the same bits with the placement on and off (8 kv heads: the pairs
+    divide evenly over the XCDs, and the sequences are split)."""
+    announce(f"attention XCD placement hq={hq} lens={lens[:4]}")
+    case = attn_cases.random_case(120 + hq + len(lens), hq, 8, 128, 16, lens, extra_pages=3)
+    monkeypatch.setenv("WQ_ATTN_XCD_LOCAL", "1")
+    on = gpu_attention(case)
+    monkeypatch.setenv("WQ_ATTN_XCD_LOCAL", "0")
+    off = gpu_attention(case)
+    assert np.array_equal(on.view(np.uint16), off.view(np.uint16))
+    check_tolerance(case, on, "XCD placement")
+
+
 def test_attention_shared_workspace_across_shapes():
     """One workspace serves consecutive calls of different shapes."""
     import torch
