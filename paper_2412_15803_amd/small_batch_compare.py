@@ -87,7 +87,7 @@ def summarise(trace_dir, out):
     launches = [r for r in rows if "gemv_mb_kernel" in r["Kernel_Name"] or "gemm_mfma_kernel" in r["Kernel_Name"]]
     launches.sort(key=lambda r: int(r["Start_Timestamp"]))
     lines = ["# Small batches: vector-ALU kernel against matrix-core kernel", "",
-             "Commands (from /tmp with TMPDIR=/tmp, one MI355X):", "", "```",
+             "Commands (from /tmp with TMPDIR=/tmp and PYTHONPATH=<repo>, one MI355X):", "", "```",
              "rocprofv3 --kernel-trace --output-format csv -d <out> -o trace -- "
              "python3 -m paper_2412_15803_amd.small_batch_compare",
              "python -m paper_2412_15803_amd.small_batch_compare --summarise <out> --out profiles/small_batch_paths.md",
